@@ -1,0 +1,201 @@
+/*
+ * da2.h - C ABI of the DraftAttention2 hot path on AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "DraftAttention2: Fast Video Diffusion with Low-Resolution-Guided
+ * Mixed-Precision Attention". One attention layer is computed in four calls,
+ * all asynchronous on a caller-given HIP stream:
+ *
+ *   da2_draft_map      pooled draft attention map            (descriptor eq., Def. 3.1)
+ *   da2_rank_assign    shared ranking into 8-bit/4-bit/skip  (Algorithm 1, routing appendix)
+ *   da2_prep_operands  per-block INT8 / E4M3 / NVFP4 operands (format appendix, NVFP4 eqs.)
+ *   da2_mixed_attn     one phased mixed-precision attention   (phased execution,
+ *                      kernel with shared softmax state       precision-state-conversion eq.)
+ *
+ * Conventions for every call
+ * --------------------------
+ * - Regions are 8x8 spatial tiles of each frame (capacity C = 64 tokens).
+ *   Tokens are numbered frame-major raster: n = t*Hg*Wg + y*Wg + x. Block
+ *   a = (t*nI + i)*nJ + j with nI = ceil(Hg/8), nJ = ceil(Wg/8); R = T*nI*nJ
+ *   blocks, Npad = 64*R slots. The slots of a block hold its valid tokens in
+ *   row-major order, then padding.
+ * - Every device buffer is allocated and owned by the caller; sizes come from
+ *   da2_sizes(). The library never allocates or frees device memory, never
+ *   synchronizes the host and keeps no mutable global state. Buffers that a
+ *   call writes must not be read or written by other work on other streams
+ *   until the call has completed on its stream.
+ * - "device" pointers must be device-accessible (hipMalloc / torch cuda
+ *   tensors); "host" pointers are ordinary process memory.
+ * - Every entry point validates its arguments on the host before touching the
+ *   GPU and returns a da2_status; no C++ exception crosses this interface.
+ *   Launch failures return DA2_ERR_HIP. Nothing is written when validation
+ *   fails.
+ * - Only gfx950 devices are supported (DA2_ERR_UNSUPPORTED otherwise). Head
+ *   dimension d must be 64 or 128.
+ */
+#ifndef DA2_H
+#define DA2_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DA2_OK = 0,
+  DA2_ERR_INVALID_ARG = -1, /* a null pointer, a bad size or an out-of-range value   */
+  DA2_ERR_UNSUPPORTED = -2, /* valid request the library does not implement / no gfx950 */
+  DA2_ERR_WORKSPACE = -3,   /* workspace smaller than da2_sizes() asks for           */
+  DA2_ERR_HIP = -4          /* the HIP runtime reported an error (launch or query)   */
+} da2_status;
+
+typedef enum { DA2_BF16 = 0, DA2_FP32 = 1 } da2_dtype;
+typedef enum { DA2_SCOPE_HEAD = 0, DA2_SCOPE_ROW = 1 } da2_scope;
+
+/* Problem shape: batch B, heads H, head dim d, latent grid T x Hg x Wg
+ * (N = T*Hg*Wg tokens). */
+typedef struct {
+  int32_t B, H, d, T, Hg, Wg;
+} da2_problem;
+
+/* A [B, H, N, d] tensor with d contiguous; strides are in elements. */
+typedef struct {
+  int64_t stride_b, stride_h, stride_n;
+  int32_t dtype; /* da2_dtype */
+  int32_t reserved;
+} da2_tensor;
+
+/* Byte sizes of the caller-allocated device buffers of one problem. */
+typedef struct {
+  int32_t R, Npad;
+  int64_t layout_bytes; /* int32 index maps, see da2_layout_build        */
+  int64_t A_bytes;      /* float32 draft map [B,H,R,R]                    */
+  int64_t cls_bytes;    /* uint8 precision map [B,H,R,R]                  */
+  int64_t stats_bytes;  /* per-head amax statistics                       */
+  int64_t lists_bytes;  /* per-row key-block lists, counts, work order    */
+  int64_t ops_bytes;    /* encoded operands                               */
+  int64_t ws_draft_bytes, ws_rank_bytes, ws_prep_bytes;
+} da2_sizes_t;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* da2_status_string(int32_t status);
+
+/* Host only. Fills *out for problem p; ranking scope affects ws_rank_bytes.
+ * Errors: INVALID_ARG for non-positive dims, d not in {64,128}, or sizes that
+ * overflow the index types (R > 65535 blocks, B*H*R > 2^31-1). */
+int32_t da2_sizes(const da2_problem* p, int32_t scope, da2_sizes_t* out);
+
+/* Host only: region layout (fused-preparation section: each region packed
+ * into one contiguous block, valid counts n_a, inverse index map).
+ * host_layout receives layout_bytes/4 int32 values:
+ *   [0, R)            n_a        valid tokens of block a (1..64)
+ *   [R, R+Npad)       slot2tok   token of each slot, -1 for padding
+ *   [R+Npad, +N)      tok2slot   slot of each token
+ * Copy it to a device buffer of layout_bytes for the compute calls. */
+int32_t da2_layout_build(const da2_problem* p, int32_t* host_layout, int64_t n_ints);
+
+/* Draft map (descriptor equation; Definition 3.1):
+ *   Qbar_a = mean, Qmax_a = channel max of Q over the valid tokens of block a
+ *   (K alike), A = (1-lambda) softmax_row(Qbar Kbar^T/sqrt d)
+ *                 + lambda softmax_row(Qmax Kmax^T/sqrt d),
+ * pooling, logits and softmax in float64, A rounded once to float32.
+ *   Q, K     device, [B,H,N,d] per *qk (bf16 or fp32)
+ *   layout   device, as built by da2_layout_build
+ *   lambda   in [0, 1]
+ *   A        device out, float32 [B,H,R,R] row-major (row = query block)
+ *   stats    device out, stats_bytes: uint32 [B*H][4 + d]; entry 0/1 hold the
+ *            float32 bit patterns of max|Q|, max|K| of each head (entries 2..
+ *            are written by da2_prep_operands)
+ *   ws       device scratch of ws_draft_bytes (see da2_ws_draft_offsets). */
+int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const int32_t* layout,
+                      const da2_problem* p, double lambda, float* A, void* stats, void* ws,
+                      int64_t ws_bytes, void* stream);
+
+/* Offsets (bytes) inside ws_draft of: [0] Qbar, [1] Qmax, [2] Kbar, [3] Kmax
+ * (float64 [B,H,R,d] each), [4] S_avg, [5] S_max (float64 [B,H,R,R] logits). */
+int32_t da2_ws_draft_offsets(const da2_problem* p, int64_t* offsets6);
+
+/* Shared ranking (Algorithm 1 without the 16-bit quota; routing appendix).
+ * Quotas from budgets num8/den and num4/den over M = R*R pairs per head
+ * (DA2_SCOPE_HEAD) or M = R pairs per query block (DA2_SCOPE_ROW):
+ *   T8 = floor(num8*M/den + 1/2), T4 = floor((num8+num4)*M/den + 1/2) - T8.
+ * Pairs are ranked by (A descending, pair index ascending) with pair index
+ * a*R+b (head) or b (row); ranks [0,T8) -> 8, [T8,T8+T4) -> 4, others -> 0.
+ *   A      device float32 [B,H,R,R] (e.g. from da2_draft_map)
+ *   cls    device out, uint8 [B,H,R,R] in {0,4,8}
+ *   lists  device out, lists_bytes (see da2_lists_offsets)
+ * Errors: INVALID_ARG if den <= 0, num8 < 0, num4 < 0, num8+num4 > den, or
+ * head scope with R*R >= 2^22. */
+int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num8, int32_t num4,
+                        int32_t den, int32_t scope, uint8_t* cls, void* lists, void* ws,
+                        int64_t ws_bytes, void* stream);
+
+/* Offsets (bytes) inside lists:
+ *   [0] keys   uint16 [B*H*R][R]: row (b,h,a) holds its 4-bit key blocks
+ *              ascending in [0,n4), then its 8-bit key blocks ascending in
+ *              [n4, n4+n8)
+ *   [1] counts int32 [B*H*R][2] = (n4, n8)
+ *   [2] order  int32 [B*H*R]: rows (b*H+h)*R+a, most expensive first
+ *   [3] meta   int32 [8]: [0] = number of rows in order                       */
+int32_t da2_lists_offsets(const da2_problem* p, int64_t* offsets4);
+
+/* Operand preparation (format appendix; NVFP4 quantization equation):
+ *   INT8 Q, K: per block delta = f32(f32(amax/127) + 1e-7), code =
+ *     round-half-away(f32(x * f32(1/delta))).
+ *   E4M3 V: per (b,h,channel) delta_c = f32(amax_c / 2.25) over all valid
+ *     keys, code = E4M3_rne(f32(v * f32(1/delta_c))); zero channels -> 0.
+ *   NVFP4 Q, K (16-channel groups) and V (16 key slots per channel):
+ *     g = f32(amax_head / 2688) (1 if zero), sigma = E4M3_rne(f32(amax_G /
+ *     f32(6 g))), e = E2M1_rne(f32(x * f32(1 / f32(g sigma)))); sigma == 0 ->
+ *     zeros. Stored as the exact fp16 value sigma*e (gfx950 has no MFMA that
+ *     applies E4M3 scales per 16 elements; sigma*e has at most 6 significant
+ *     bits, so fp16 holds it exactly and fp16 MFMA reproduces the products).
+ * Casts round to nearest even and saturate; padding slots encode to zero.
+ *   Q, K, V  device [B,H,N,d] per *qkv; stats from da2_draft_map (this call
+ *            fills entries 2.. : max|V| and the per-channel max|V_c|)
+ *   ops      device out, ops_bytes (see da2_ops_offsets)                   */
+int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv,
+                          const int32_t* layout, const da2_problem* p, void* stats, void* ops,
+                          void* ws, int64_t ws_bytes, void* stream);
+
+/* Offsets (bytes) inside ops, per section; each section is [B*H][R][...]
+ * with one 64-slot block per R, in the fragment order of the gfx950 MFMA
+ * tiles the attention kernel consumes (lane = 0..63, g = lane/32):
+ *   [0] Q4  fp16 [qt:2][s:d/16][lane][8]  = sigma*e of Q[slot 32qt+lane%32][16s+8g+e]
+ *   [1] K4  fp16 [j:2][s:d/16][lane][8]   = sigma*e of K[kappa(j,lane%32)][16s+8g+e]
+ *   [2] V4  fp16 [t:d/32][s:4][lane][8]   = sigma*e of V[32(s/2)+16g+8(s%2)+e][32t+lane%32]
+ *   [3] Q8  int8 [qt:2][s:d/32][lane][16] = code of Q[slot 32qt+lane%32][32s+16g+e]
+ *   [4] K8  int8 [j:2][s:d/32][lane][16]  = code of K[kappa(j,lane%32)][32s+16g+e]
+ *   [5] V8  e4m3 [t:d/32][h:2][lane][16]  = code of V[32h+16g+e][32t+lane%32]
+ *   [6] dQ  float32 [B*H][R]   INT8 scale of each query block
+ *   [7] dK  float32 [B*H][R]   INT8 scale of each key block
+ *   [8] dV  float32 [B*H][d]   E4M3 per-channel scale of V
+ *   [9] g   float32 [B*H][4]   (g_Q, g_K, g_V, 0) NVFP4 tensor scales
+ * with kappa(j, r) = 32j + 16((r/4)%2) + 4(r/8) + r%4 (the key permutation
+ * that puts each 16-slot group of a query row into one lane, see the operand
+ * permutation equation). */
+int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets10);
+
+/* Phased mixed-precision attention (phased-execution appendix;
+ * precision-state-conversion equation). For each query block a (one wave,
+ * 64 query slots) the NVFP4 key blocks are processed in ascending order, then
+ * the INT8 ones, sharing fp32 row maxima m, denominator l and numerator U:
+ *   s = Qhat Khat^T / sqrt d; m_j = max(m_{j-1}, rowmax_j s); Pt = exp(s - m_j)
+ *   4-bit: l += sum Pt; sigma_P = E4M3(448 max_16 Pt); U += (sigma_P/2688)
+ *          E2M1(2688 Pt/sigma_P) Vhat4 (fp16 MFMA on sigma*e operands)
+ *   Enter: U_c /= eta delta_c, l /= eta   (eta = 2^-8.807)
+ *   8-bit: int8 MFMA logits; P = 2^((s - m) log2 e + 8.807); l += sum P;
+ *          U += E4M3(P) V8 (fp8 MFMA)
+ *   Exit:  U_c *= eta delta_c, l *= eta;  O = U / l (0 if no retained block)
+ * and the rows are written to token order through slot2tok.
+ *   ops, lists, layout  device, from the calls above
+ *   out      descriptor of O (dtype fp32 or bf16)
+ *   O        device out [B,H,N,d]; every token row is written.               */
+int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout,
+                       const da2_problem* p, const da2_tensor* out, void* O, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DA2_H */

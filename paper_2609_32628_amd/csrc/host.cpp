@@ -1,0 +1,364 @@
+// Host side of libda2: argument validation, buffer sizes and offsets, the region
+// layout and the four stream-ordered entry points. Validation never touches the
+// GPU, so every error path can be exercised on a machine without one.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstring>
+
+#include "../../include/da2.h"
+#include "launch.hpp"
+
+namespace {
+
+constexpr int64_t kAlign = 256;
+inline int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Dims {
+  int64_t B, H, d, T, Hg, Wg, N, R, Npad, BH;
+};
+
+int32_t derive(const da2_problem* p, Dims* o) {
+  if (!p) return DA2_ERR_INVALID_ARG;
+  if (p->B <= 0 || p->H <= 0 || p->T <= 0 || p->Hg <= 0 || p->Wg <= 0 || p->d <= 0) return DA2_ERR_INVALID_ARG;
+  if (p->d != 64 && p->d != 128) return DA2_ERR_INVALID_ARG;
+  Dims d{};
+  d.B = p->B;
+  d.H = p->H;
+  d.d = p->d;
+  d.T = p->T;
+  d.Hg = p->Hg;
+  d.Wg = p->Wg;
+  d.N = d.T * d.Hg * d.Wg;
+  d.R = d.T * ((d.Hg + 7) / 8) * ((d.Wg + 7) / 8);
+  d.Npad = 64 * d.R;
+  d.BH = d.B * d.H;
+  if (d.R > 65535 || d.N > (1ll << 31) - 1 || d.BH * d.R > (1ll << 31) - 1) return DA2_ERR_INVALID_ARG;
+  *o = d;
+  return DA2_OK;
+}
+
+void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
+  std::memset(s, 0, sizeof(*s));
+  s->R = (int32_t)d.R;
+  s->Npad = (int32_t)d.Npad;
+  s->layout_bytes = 4 * (d.R + d.Npad + d.N);
+  s->A_bytes = 4 * d.BH * d.R * d.R;
+  s->cls_bytes = d.BH * d.R * d.R;
+  s->stats_bytes = 4 * d.BH * (4 + d.d);
+  s->lists_bytes = align_up(2 * d.BH * d.R * d.R) + align_up(8 * d.BH * d.R) + align_up(4 * d.BH * d.R) + kAlign;
+  const int64_t e = d.BH * d.Npad * d.d;
+  s->ops_bytes = 3 * align_up(2 * e) + 3 * align_up(e) + 2 * align_up(4 * d.BH * d.R) + align_up(4 * d.BH * d.d) +
+                 align_up(16 * d.BH);
+  s->ws_draft_bytes = 4 * align_up(8 * d.BH * d.R * d.d) + 2 * align_up(8 * d.BH * d.R * d.R);
+  int64_t thr = scope == DA2_SCOPE_ROW ? 16 * d.BH * d.R : 16 * d.BH;
+  s->ws_rank_bytes = align_up(4 * d.BH * 2 * 2048) + align_up(thr) + align_up(16 * d.BH) + align_up(16 * d.BH) +
+                     align_up(4 * d.BH * d.R);
+  s->ws_prep_bytes = 0;
+}
+
+void ops_offsets(const Dims& d, int64_t* off) {
+  const int64_t e = d.BH * d.Npad * d.d;
+  int64_t o = 0;
+  const int64_t sz[10] = {2 * e, 2 * e, 2 * e, e, e, e, 4 * d.BH * d.R, 4 * d.BH * d.R, 4 * d.BH * d.d, 16 * d.BH};
+  for (int i = 0; i < 10; ++i) {
+    off[i] = o;
+    o += align_up(sz[i]);
+  }
+}
+
+void lists_offsets(const Dims& d, int64_t* off) {
+  off[0] = 0;
+  off[1] = align_up(2 * d.BH * d.R * d.R);
+  off[2] = off[1] + align_up(8 * d.BH * d.R);
+  off[3] = off[2] + align_up(4 * d.BH * d.R);
+}
+
+void draft_offsets(const Dims& d, int64_t* off) {
+  const int64_t pooled = align_up(8 * d.BH * d.R * d.d), logits = align_up(8 * d.BH * d.R * d.R);
+  for (int i = 0; i < 4; ++i) off[i] = i * pooled;
+  off[4] = 4 * pooled;
+  off[5] = 4 * pooled + logits;
+}
+
+int32_t check_tensor(const da2_tensor* t, const Dims& d, bool out) {
+  if (!t) return DA2_ERR_INVALID_ARG;
+  if (t->dtype != DA2_BF16 && t->dtype != DA2_FP32) return DA2_ERR_INVALID_ARG;
+  if (t->stride_b <= 0 || t->stride_h <= 0 || t->stride_n <= 0) return DA2_ERR_INVALID_ARG;
+  if (t->stride_n < d.d) return DA2_ERR_INVALID_ARG;
+  (void)out;
+  return DA2_OK;
+}
+
+// gfx950 check, cached per device ordinal (0 unknown, 1 ok, 2 unsupported).
+std::atomic<int8_t> g_arch_ok[64];
+
+int32_t check_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return DA2_ERR_UNSUPPORTED;
+  if (dev < 64) {
+    int8_t c = g_arch_ok[dev].load(std::memory_order_relaxed);
+    if (c == 1) return DA2_OK;
+    if (c == 2) return DA2_ERR_UNSUPPORTED;
+  }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return DA2_ERR_HIP;
+  const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+  if (dev < 64) g_arch_ok[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
+  return ok ? DA2_OK : DA2_ERR_UNSUPPORTED;
+}
+
+int32_t hip_status(hipError_t e) { return e == hipSuccess ? DA2_OK : DA2_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* da2_status_string(int32_t s) {
+  switch (s) {
+    case DA2_OK: return "DA2_OK";
+    case DA2_ERR_INVALID_ARG: return "DA2_ERR_INVALID_ARG: invalid argument";
+    case DA2_ERR_UNSUPPORTED: return "DA2_ERR_UNSUPPORTED: unsupported request or device (gfx950 required)";
+    case DA2_ERR_WORKSPACE: return "DA2_ERR_WORKSPACE: workspace too small";
+    case DA2_ERR_HIP: return "DA2_ERR_HIP: HIP runtime error";
+    default: return "DA2 unknown status";
+  }
+}
+
+int32_t da2_sizes(const da2_problem* p, int32_t scope, da2_sizes_t* out) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if (!out || (scope != DA2_SCOPE_HEAD && scope != DA2_SCOPE_ROW)) return DA2_ERR_INVALID_ARG;
+  sizes_of(d, scope, out);
+  return DA2_OK;
+}
+
+int32_t da2_ws_draft_offsets(const da2_problem* p, int64_t* off) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if (!off) return DA2_ERR_INVALID_ARG;
+  draft_offsets(d, off);
+  return DA2_OK;
+}
+
+int32_t da2_lists_offsets(const da2_problem* p, int64_t* off) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if (!off) return DA2_ERR_INVALID_ARG;
+  lists_offsets(d, off);
+  return DA2_OK;
+}
+
+int32_t da2_ops_offsets(const da2_problem* p, int64_t* off) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if (!off) return DA2_ERR_INVALID_ARG;
+  ops_offsets(d, off);
+  return DA2_OK;
+}
+
+int32_t da2_layout_build(const da2_problem* p, int32_t* L, int64_t n_ints) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if (!L || n_ints < d.R + d.Npad + d.N) return DA2_ERR_INVALID_ARG;
+  const int64_t nI = (d.Hg + 7) / 8, nJ = (d.Wg + 7) / 8;
+  int32_t* n_a = L;
+  int32_t* s2t = L + d.R;
+  int32_t* t2s = L + d.R + d.Npad;
+  for (int64_t i = 0; i < d.Npad; ++i) s2t[i] = -1;
+  for (int64_t t = 0; t < d.T; ++t)
+    for (int64_t i = 0; i < nI; ++i)
+      for (int64_t j = 0; j < nJ; ++j) {
+        const int64_t a = (t * nI + i) * nJ + j;
+        const int64_t y1 = i * 8 + 8 < d.Hg ? i * 8 + 8 : d.Hg, x1 = j * 8 + 8 < d.Wg ? j * 8 + 8 : d.Wg;
+        int32_t s = 0;
+        for (int64_t y = i * 8; y < y1; ++y)
+          for (int64_t x = j * 8; x < x1; ++x) {
+            const int64_t tok = t * d.Hg * d.Wg + y * d.Wg + x;
+            s2t[a * 64 + s] = (int32_t)tok;
+            t2s[tok] = (int32_t)(a * 64 + s);
+            ++s;
+          }
+        n_a[a] = s;
+      }
+  return DA2_OK;
+}
+
+int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const int32_t* layout,
+                      const da2_problem* p, double lambda, float* A, void* stats, void* ws, int64_t ws_bytes,
+                      void* stream) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if ((st = check_tensor(qk, d, false))) return st;
+  if (!Q || !K || !layout || !A || !stats || !ws) return DA2_ERR_INVALID_ARG;
+  if (!(lambda >= 0.0 && lambda <= 1.0)) return DA2_ERR_INVALID_ARG;
+  da2_sizes_t sz;
+  sizes_of(d, DA2_SCOPE_HEAD, &sz);
+  if (ws_bytes < sz.ws_draft_bytes) return DA2_ERR_WORKSPACE;
+  if ((st = check_device())) return st;
+  int64_t off[6];
+  draft_offsets(d, off);
+  char* w = static_cast<char*>(ws);
+  da2::DraftArgs a{};
+  a.Q = Q;
+  a.K = K;
+  a.sb = qk->stride_b;
+  a.sh = qk->stride_h;
+  a.sn = qk->stride_n;
+  a.dtype = qk->dtype;
+  a.B = (int)d.B;
+  a.H = (int)d.H;
+  a.d = (int)d.d;
+  a.R = (int)d.R;
+  a.Npad = (int)d.Npad;
+  a.layout = layout;
+  a.lambda = lambda;
+  a.A = A;
+  a.stats = static_cast<uint32_t*>(stats);
+  a.Qbar = reinterpret_cast<double*>(w + off[0]);
+  a.Qmax = reinterpret_cast<double*>(w + off[1]);
+  a.Kbar = reinterpret_cast<double*>(w + off[2]);
+  a.Kmax = reinterpret_cast<double*>(w + off[3]);
+  a.S1 = reinterpret_cast<double*>(w + off[4]);
+  a.S2 = reinterpret_cast<double*>(w + off[5]);
+  return hip_status(da2::launch_draft(a, static_cast<hipStream_t>(stream)));
+}
+
+int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num8, int32_t num4, int32_t den,
+                        int32_t scope, uint8_t* cls, void* lists, void* ws, int64_t ws_bytes, void* stream) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if (!A || !cls || !lists || !ws) return DA2_ERR_INVALID_ARG;
+  if (den <= 0 || num8 < 0 || num4 < 0 || (int64_t)num8 + num4 > den) return DA2_ERR_INVALID_ARG;
+  if (scope != DA2_SCOPE_HEAD && scope != DA2_SCOPE_ROW) return DA2_ERR_INVALID_ARG;
+  if (scope == DA2_SCOPE_HEAD && d.R * d.R >= (1ll << 22)) return DA2_ERR_INVALID_ARG;
+  if (scope == DA2_SCOPE_ROW && d.R > 8192) return DA2_ERR_UNSUPPORTED;
+  da2_sizes_t sz;
+  sizes_of(d, scope, &sz);
+  if (ws_bytes < sz.ws_rank_bytes) return DA2_ERR_WORKSPACE;
+  if ((st = check_device())) return st;
+  const int64_t M = scope == DA2_SCOPE_HEAD ? d.R * d.R : d.R;
+  const int64_t c8 = (2 * (int64_t)num8 * M + den) / (2 * (int64_t)den);
+  const int64_t c84 = (2 * ((int64_t)num8 + num4) * M + den) / (2 * (int64_t)den);
+  int64_t lo[4];
+  lists_offsets(d, lo);
+  char* lb = static_cast<char*>(lists);
+  char* w = static_cast<char*>(ws);
+  int64_t thr = scope == DA2_SCOPE_ROW ? 16 * d.BH * d.R : 16 * d.BH;
+  da2::RankArgs a{};
+  a.A = A;
+  a.B = (int)d.B;
+  a.H = (int)d.H;
+  a.R = (int)d.R;
+  a.scope = scope;
+  a.T8 = c8;
+  a.T4 = c84 - c8;
+  a.cls = cls;
+  a.keys = reinterpret_cast<uint16_t*>(lb + lo[0]);
+  a.counts = reinterpret_cast<int32_t*>(lb + lo[1]);
+  a.order = reinterpret_cast<int32_t*>(lb + lo[2]);
+  a.meta = reinterpret_cast<int32_t*>(lb + lo[3]);
+  int64_t o = 0;
+  a.hist = reinterpret_cast<uint32_t*>(w + o);
+  o += align_up(4 * d.BH * 2 * 2048);
+  a.thr = reinterpret_cast<uint64_t*>(w + o);
+  o += align_up(thr);
+  a.prefix = reinterpret_cast<uint64_t*>(w + o);
+  o += align_up(16 * d.BH);
+  a.kleft = reinterpret_cast<int64_t*>(w + o);
+  o += align_up(16 * d.BH);
+  a.cost = reinterpret_cast<int32_t*>(w + o);
+  return hip_status(da2::launch_rank(a, static_cast<hipStream_t>(stream)));
+}
+
+int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv, const int32_t* layout,
+                          const da2_problem* p, void* stats, void* ops, void* ws, int64_t ws_bytes, void* stream) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if ((st = check_tensor(qkv, d, false))) return st;
+  if (!Q || !K || !V || !layout || !stats || !ops) return DA2_ERR_INVALID_ARG;
+  (void)ws;
+  if (ws_bytes < 0) return DA2_ERR_WORKSPACE;
+  if ((st = check_device())) return st;
+  int64_t off[10];
+  ops_offsets(d, off);
+  char* ob = static_cast<char*>(ops);
+  da2::PrepArgs a{};
+  a.Q = Q;
+  a.K = K;
+  a.V = V;
+  a.sb = qkv->stride_b;
+  a.sh = qkv->stride_h;
+  a.sn = qkv->stride_n;
+  a.dtype = qkv->dtype;
+  a.B = (int)d.B;
+  a.H = (int)d.H;
+  a.d = (int)d.d;
+  a.R = (int)d.R;
+  a.Npad = (int)d.Npad;
+  a.layout = layout;
+  a.stats = static_cast<uint32_t*>(stats);
+  a.Q4 = reinterpret_cast<_Float16*>(ob + off[0]);
+  a.K4 = reinterpret_cast<_Float16*>(ob + off[1]);
+  a.V4 = reinterpret_cast<_Float16*>(ob + off[2]);
+  a.Q8 = reinterpret_cast<int8_t*>(ob + off[3]);
+  a.K8 = reinterpret_cast<int8_t*>(ob + off[4]);
+  a.V8 = reinterpret_cast<uint8_t*>(ob + off[5]);
+  a.dQ = reinterpret_cast<float*>(ob + off[6]);
+  a.dK = reinterpret_cast<float*>(ob + off[7]);
+  a.dV = reinterpret_cast<float*>(ob + off[8]);
+  a.g = reinterpret_cast<float*>(ob + off[9]);
+  return hip_status(da2::launch_prep(a, static_cast<hipStream_t>(stream)));
+}
+
+int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout, const da2_problem* p,
+                       const da2_tensor* out, void* O, void* stream) {
+  Dims d;
+  int32_t st = derive(p, &d);
+  if (st) return st;
+  if ((st = check_tensor(out, d, true))) return st;
+  if (!ops || !lists || !layout || !O) return DA2_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
+  int64_t off[10], lo[4];
+  ops_offsets(d, off);
+  lists_offsets(d, lo);
+  const char* ob = static_cast<const char*>(ops);
+  const char* lb = static_cast<const char*>(lists);
+  da2::AttnArgs a{};
+  a.Q4 = reinterpret_cast<const _Float16*>(ob + off[0]);
+  a.K4 = reinterpret_cast<const _Float16*>(ob + off[1]);
+  a.V4 = reinterpret_cast<const _Float16*>(ob + off[2]);
+  a.Q8 = reinterpret_cast<const int8_t*>(ob + off[3]);
+  a.K8 = reinterpret_cast<const int8_t*>(ob + off[4]);
+  a.V8 = reinterpret_cast<const uint8_t*>(ob + off[5]);
+  a.dQ = reinterpret_cast<const float*>(ob + off[6]);
+  a.dK = reinterpret_cast<const float*>(ob + off[7]);
+  a.dV = reinterpret_cast<const float*>(ob + off[8]);
+  a.g = reinterpret_cast<const float*>(ob + off[9]);
+  a.keys = reinterpret_cast<const uint16_t*>(lb + lo[0]);
+  a.counts = reinterpret_cast<const int32_t*>(lb + lo[1]);
+  a.order = reinterpret_cast<const int32_t*>(lb + lo[2]);
+  a.layout = layout;
+  a.B = (int)d.B;
+  a.H = (int)d.H;
+  a.d = (int)d.d;
+  a.R = (int)d.R;
+  a.Npad = (int)d.Npad;
+  a.O = O;
+  a.ob = out->stride_b;
+  a.oh = out->stride_h;
+  a.on = out->stride_n;
+  a.odtype = out->dtype;
+  return hip_status(da2::launch_attn(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

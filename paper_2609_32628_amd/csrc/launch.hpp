@@ -1,0 +1,77 @@
+// Kernel argument blocks and launchers shared by the host library and the
+// kernel translation units. Internal to libda2.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace da2 {
+
+struct DraftArgs {
+  const void* Q;
+  const void* K;
+  int64_t sb, sh, sn;
+  int dtype;
+  int B, H, d, R, Npad;
+  const int32_t* layout;
+  double lambda;
+  float* A;
+  uint32_t* stats;
+  double *Qbar, *Qmax, *Kbar, *Kmax, *S1, *S2;
+};
+
+struct RankArgs {
+  const float* A;
+  int B, H, R;
+  int scope;
+  int64_t T8, T4;          // quotas per head (head scope) or per row (row scope)
+  uint8_t* cls;
+  uint16_t* keys;          // lists: [BH*R][R]
+  int32_t* counts;         // [BH*R][2]
+  int32_t* order;          // [BH*R]
+  int32_t* meta;           // [8]
+  // workspace
+  uint32_t* hist;          // [BH][2][2048]
+  uint64_t* thr;           // head: [BH][2]; row: [BH*R][2]
+  uint64_t* prefix;        // [BH][2]
+  int64_t* kleft;          // [BH][2]
+  int32_t* cost;           // [BH*R]
+};
+
+struct PrepArgs {
+  const void* Q;
+  const void* K;
+  const void* V;
+  int64_t sb, sh, sn;
+  int dtype;
+  int B, H, d, R, Npad;
+  const int32_t* layout;
+  uint32_t* stats;
+  // ops sections
+  _Float16 *Q4, *K4, *V4;
+  int8_t *Q8, *K8;
+  uint8_t* V8;
+  float *dQ, *dK, *dV, *g;
+};
+
+struct AttnArgs {
+  const _Float16 *Q4, *K4, *V4;
+  const int8_t *Q8, *K8;
+  const uint8_t* V8;
+  const float *dQ, *dK, *dV, *g;
+  const uint16_t* keys;
+  const int32_t* counts;
+  const int32_t* order;
+  const int32_t* layout;
+  int B, H, d, R, Npad;
+  void* O;
+  int64_t ob, oh, on;
+  int odtype;
+};
+
+hipError_t launch_draft(const DraftArgs& args, hipStream_t stream);
+hipError_t launch_rank(const RankArgs& args, hipStream_t stream);
+hipError_t launch_prep(const PrepArgs& args, hipStream_t stream);
+hipError_t launch_attn(const AttnArgs& args, hipStream_t stream);
+
+}  // namespace da2

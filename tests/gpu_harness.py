@@ -1,0 +1,146 @@
+"""Shared helpers of the GPU parity tests: run the library's four calls through
+the C ABI, read the documented buffers back, and build the oracle's expected
+values in the same order. The oracle and the library never exchange data
+except through these comparisons (oracle inputs come from synth only)."""
+import sys
+
+import numpy as np
+import torch
+
+from oracle import encode, formats, partition, pipeline, rank
+from paper_2609_32628_amd import api
+from synth import configs, gen
+from fraglayout import to_frag
+
+TOL_MAX_ABS = 2e-2     # output tolerances of the parity bar
+TOL_REL_L2 = 5e-3
+NEAR_TIE_REL = 1e-6    # mask mismatches allowed only this close to a threshold score
+
+# A small ragged case: 3 frames of 13x21 tokens (2x3 tiles, edge tiles 40 / 24 / 15 ...).
+SMALL = configs.Workload("small-3x13x21-h2-d128", B=2, H=2, d=128, T=3, Hg=13, Wg=21, dtype="bf16",
+                         budgets=(10, 30, 100), scope="head", head_scale=True, seed=11)
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def problem_of(w):
+    return api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg)
+
+
+def inputs(w, heads=None):
+    Q, K, V = gen.generate(w, heads)
+    return Q, K, V
+
+
+def to_device(X, w):
+    t = torch.from_numpy(np.ascontiguousarray(X))
+    return t.to(torch.bfloat16 if w.dtype == "bf16" else torch.float32).cuda()
+
+
+def sections(buf, p):
+    """Encoded operands of the ops buffer as numpy arrays [BH, R, ...]."""
+    off = api.da2_ops_offsets(p)
+    raw = buf.ops.cpu().numpy()
+    BH, R, d = p.B * p.H, buf.sizes["R"], p.d
+    out = {}
+    specs = [("Q4", np.float16, (R, 64 * d)), ("K4", np.float16, (R, 64 * d)), ("V4", np.float16, (R, 64 * d)),
+             ("Q8", np.int8, (R, 64 * d)), ("K8", np.int8, (R, 64 * d)), ("V8", np.uint8, (R, 64 * d)),
+             ("dQ", np.float32, (R,)), ("dK", np.float32, (R,)), ("dV", np.float32, (d,)), ("g", np.float32, (4,))]
+    for i, (name, dt, shape) in enumerate(specs):
+        nbytes = BH * int(np.prod(shape)) * np.dtype(dt).itemsize
+        out[name] = raw[off[i]:off[i] + nbytes].view(dt).reshape((BH,) + shape)
+    return out
+
+
+def lists_of(buf, p):
+    lo = api.da2_lists_offsets(p)
+    raw = buf.lists.cpu().numpy()
+    BH, R = p.B * p.H, buf.sizes["R"]
+    keys = raw[lo[0]:lo[0] + 2 * BH * R * R].view(np.uint16).reshape(BH * R, R)
+    counts = raw[lo[1]:lo[1] + 8 * BH * R].view(np.int32).reshape(BH * R, 2)
+    order = raw[lo[2]:lo[2] + 4 * BH * R].view(np.int32)
+    return keys, counts, order
+
+
+def write_lists(buf, p, cls_all):
+    """Oracle class maps [BH, R, R] -> the lists section (identity work order)."""
+    lo = api.da2_lists_offsets(p)
+    BH, R = cls_all.shape[0], cls_all.shape[1]
+    keys = np.zeros((BH * R, R), np.uint16)
+    counts = np.zeros((BH * R, 2), np.int32)
+    for i, row in enumerate(cls_all.reshape(BH * R, R)):
+        l4, l8 = rank.key_lists(row)
+        keys[i, :l4.size] = l4
+        keys[i, l4.size:l4.size + l8.size] = l8
+        counts[i] = (l4.size, l8.size)
+    raw = buf.lists.cpu().numpy()
+    raw[lo[0]:lo[0] + keys.nbytes] = keys.view(np.uint8).reshape(-1)
+    raw[lo[1]:lo[1] + counts.nbytes] = counts.view(np.uint8).reshape(-1)
+    order = np.arange(BH * R, dtype=np.int32)
+    raw[lo[2]:lo[2] + order.nbytes] = order.view(np.uint8)
+    buf.lists.copy_(torch.from_numpy(raw))
+
+
+def expected_sections(enc):
+    """Oracle encodings of one head in the ops-buffer order."""
+    sQ = np.repeat(enc["sQ"], 16, axis=2) * enc["eQ"]
+    sK = np.repeat(enc["sK"], 16, axis=2) * enc["eK"]
+    sV = np.repeat(enc["sV"], 16, axis=1) * enc["eV"]
+    return {
+        "Q4": to_frag("Q4", sQ), "K4": to_frag("K4", sK), "V4": to_frag("V4", sV),
+        "Q8": to_frag("Q8", enc["q8"]), "K8": to_frag("K8", enc["k8"]),
+        "V8": to_frag("V8", formats.e4m3_code(enc["v8"])),
+        "dQ": enc["dQ"], "dK": enc["dK"], "dV": enc["dV"],
+        "g": np.array([enc["gQ"], enc["gK"], enc["gV"], 0], np.float32),
+    }
+
+
+def write_ops(buf, p, encs):
+    """Oracle encodings of every head -> the ops buffer (stage injection)."""
+    off = api.da2_ops_offsets(p)
+    raw = buf.ops.cpu().numpy()
+    order = ["Q4", "K4", "V4", "Q8", "K8", "V8", "dQ", "dK", "dV", "g"]
+    for i, name in enumerate(order):
+        arr = np.stack([expected_sections(e)[name] for e in encs])
+        b = np.ascontiguousarray(arr).view(np.uint8).reshape(-1)
+        raw[off[i]:off[i] + b.size] = b
+    buf.ops.copy_(torch.from_numpy(raw))
+
+
+def compare_outputs(O_gpu, O_ref, label):
+    """Parity bar on the rows where O_ref is defined (not NaN)."""
+    rows = ~np.isnan(O_ref).any(axis=-1)
+    a, b = O_gpu[rows].astype(np.float64), O_ref[rows]
+    err = np.abs(a - b)
+    max_abs = float(err.max()) if err.size else 0.0
+    rel = float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+    log(f"[{label}] rows={int(rows.sum())} max_abs={max_abs:.3e} rel_l2={rel:.3e}")
+    assert max_abs <= TOL_MAX_ABS, (label, max_abs)
+    assert rel <= TOL_REL_L2, (label, rel)
+    return max_abs, rel
+
+
+def mask_mismatches(cls_gpu, cls_ref, A_ref, T8, T4, scope):
+    """Count class mismatches; every one must be a near-tie at the threshold it crossed."""
+    bad = np.nonzero(cls_gpu != cls_ref)
+    if bad[0].size == 0:
+        return 0
+    R = A_ref.shape[0]
+    if scope == "head":
+        flat = A_ref.reshape(-1).astype(np.float64)
+        order = np.lexsort((np.arange(flat.size), -flat))
+        thetas = [flat[order[k - 1]] for k in (T8, T8 + T4) if k > 0]
+        for a, b in zip(*bad):
+            s = float(A_ref[a, b])
+            assert min(abs(s - t) / abs(t) for t in thetas) <= NEAR_TIE_REL, (a, b, s, thetas)
+    else:
+        for a, b in zip(*bad):
+            row = A_ref[a].astype(np.float64)
+            order = np.lexsort((np.arange(R), -row))
+            thetas = [row[order[k - 1]] for k in (T8, T8 + T4) if k > 0]
+            s = float(A_ref[a, b])
+            assert min(abs(s - t) / abs(t) for t in thetas) <= NEAR_TIE_REL, (a, b, s, thetas)
+    return bad[0].size
