@@ -32,6 +32,22 @@ def _compile(src):
     return obj
 
 
+PROBE_SRC = os.path.join(os.path.dirname(HERE), "tests", "probes", "fmt_probe.hip")
+PROBE_OUT = os.path.join(os.path.dirname(HERE), "tests", "probes", "libda2_probe.so")
+
+
+def build_probe():
+    """Device format probe used by the GPU tests (test infrastructure)."""
+    if not os.path.exists(PROBE_SRC):
+        return None
+    cmd = [HIPCC, *FLAGS, "-x", "hip", "-shared", PROBE_SRC, "-o", PROBE_OUT + ".tmp"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for the probe:\n{r.stdout}\n{r.stderr}")
+    os.replace(PROBE_OUT + ".tmp", PROBE_OUT)
+    return PROBE_OUT
+
+
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
@@ -42,6 +58,7 @@ def build(verbose=False):
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, OUT)
+    build_probe()
     if verbose:
         print("built", OUT)
     return OUT

@@ -20,6 +20,16 @@
 // 2688/g_V and l the unamplified weights; Enter converts to the 8-bit path's
 // units U_c / (eta delta_c), l / eta; the 8-bit phase accumulates amplified
 // weights 2^(z - m + 8.807) and E4M3 codes; Exit converts back.
+//
+// Latency: each block's V fragments are requested before its QK^T product and
+// the next block's K fragments right after it, so both loads are in flight
+// while the softmax runs. The query fragments sit in LDS (read once per block)
+// to leave registers for these prefetches.
+//
+// Weight conversions use the gfx950 instructions v_cvt_pk_fp8_f32 (E4M3) and
+// v_cvt_scalef32_pk_fp4_f32 / v_cvt_scalef32_pk_f16_fp4 (E2M1 and back, unit
+// scales); both round to nearest even, which the device format tests check
+// against the format definitions.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -29,6 +39,16 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kExpOffset = 8.807f;
 
 __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// Asynchronous copy of one 1 KB operand fragment (16 bytes per lane, lane
+// order) from global memory to LDS at the wave-uniform address dst.
+__device__ inline void dma_fragment(const void* src_lane, void* dst) {
+  __builtin_amdgcn_global_load_lds(src_lane, (lds_ptr)dst, 16, 0, 0);
+}
+__device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ inline void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 template <int NT>
 __device__ inline void rescale(f32x16 (&U)[NT], float alpha) {
@@ -41,7 +61,7 @@ __device__ inline void rescale(f32x16 (&U)[NT], float alpha) {
 // Rescales l and U by 2^(m_old - m_new) and returns m_new.
 template <int NT>
 __device__ inline float update_max(float bm_in, float scale, float& m, float& l, f32x16 (&U)[NT]) {
-  float bm = fmaxf(bm_in, __shfl_xor(bm_in, 32, 64));
+  const float bm = fmaxf(bm_in, __shfl_xor(bm_in, 32, 64));
   const float mn = fmaxf(m, bm * scale);
   const float alpha = exp2_fast(m - mn);
   m = mn;
@@ -50,12 +70,62 @@ __device__ inline float update_max(float bm_in, float scale, float& m, float& l,
   return mn;
 }
 
+__device__ inline float max16(const f32x16& v) {
+  float a = fmaxf(fmaxf(v[0], v[1]), v[2]), b = fmaxf(fmaxf(v[3], v[4]), v[5]);
+  float c = fmaxf(fmaxf(v[6], v[7]), v[8]), d = fmaxf(fmaxf(v[9], v[10]), v[11]);
+  float e = fmaxf(fmaxf(v[12], v[13]), v[14]);
+  return fmaxf(fmaxf(fmaxf(a, b), fmaxf(c, d)), fmaxf(e, v[15]));
+}
+
+// NVFP4 weights of one 16-slot group held by this lane (slots of S[0..15]):
+// sigma_P = E4M3(448 max Pt), w = sigma_P * E2M1(Pt * 2688 / sigma_P) as fp16
+// pairs for the P^T operand; returns the fp32 sum of Pt.
+__device__ inline float nvfp4_weights(const f32x16& S, float c, float mn, float gmax, f16x8& lo, f16x8& hi) {
+  const float pmax = exp2_fast(__builtin_fmaf(gmax, c, -mn));
+  const float sigma = e4m3_round_mag(fminf(448.0f * pmax, 448.0f));
+  const float rs = sigma > 0.0f ? 2688.0f * __builtin_amdgcn_rcpf(sigma) : 0.0f;
+  const _Float16 sh = (_Float16)sigma;
+  const f16x2 s2 = {sh, sh};
+  float p[16];
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    p[i] = exp2_fast(__builtin_fmaf(S[i], c, -mn));
+    sum += p[i];
+    p[i] *= rs;
+  }
+  // E2M1 codes, two per byte (byte selector must be a literal)
+  uint32_t f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, p[0], p[1], 1.0f, 0);
+  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, p[2], p[3], 1.0f, 1);
+  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, p[4], p[5], 1.0f, 2);
+  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, p[6], p[7], 1.0f, 3);
+  uint32_t f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, p[8], p[9], 1.0f, 0);
+  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, p[10], p[11], 1.0f, 1);
+  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, p[12], p[13], 1.0f, 2);
+  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, p[14], p[15], 1.0f, 3);
+  // back to fp16 and times sigma_P (exact: at most 6 significant bits)
+  const f16x2 a0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 0) * s2;
+  const f16x2 a1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 1) * s2;
+  const f16x2 a2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 2) * s2;
+  const f16x2 a3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 3) * s2;
+  const f16x2 b0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f1, 1.0f, 0) * s2;
+  const f16x2 b1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f1, 1.0f, 1) * s2;
+  const f16x2 b2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f1, 1.0f, 2) * s2;
+  const f16x2 b3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f1, 1.0f, 3) * s2;
+  lo = f16x8{a0[0], a0[1], a1[0], a1[1], a2[0], a2[1], a3[0], a3[1]};
+  hi = f16x8{b0[0], b0[1], b1[0], b1[1], b2[0], b2[1], b3[0], b3[1]};
+  return sum;
+}
+
 template <int D>
 __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
   constexpr int NS16 = D / 16, NS32 = D / 32, NT = D / 32;
+  __shared__ f16x8 sQ[2 * NS16 * 64];  // query fragments of the current phase (16 KB at d=128)
+  __shared__ f16x8 sK[2 * NS16 * 64];  // key fragments of the next block (DMA target)
   const int lane = threadIdx.x, r = lane & 31, g = lane >> 5;
   const int R = args.R;
   const int item = args.order[blockIdx.x];
+  if (item < 0) return;
   const int bh = item / R, a = item % R;
   const Layout L = layout_view(args.layout, R, args.Npad);
   const int n4 = args.counts[2 * item], n8 = args.counts[2 * item + 1];
@@ -74,70 +144,75 @@ __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
   // ------------------------------ NVFP4 phase ------------------------------
   if (n4 > 0) {
     const float c4 = args.g[bh * 4 + 0] * args.g[bh * 4 + 1] * kLog2e * rsqd;
-    f16x8 Qf[2][NS16];
-    const _Float16* Qa = args.Q4 + (blk0 + a) * (int64_t)kCap * D;
+    const f16x8* Qa = reinterpret_cast<const f16x8*>(args.Q4) + (blk0 + a) * (kCap * D / 8);
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int c = 0; c < 2 * NS16; ++c) sQ[c * 64 + lane] = Qa[c * 64 + lane];
+    const f16x8* K4 = reinterpret_cast<const f16x8*>(args.K4);
+    const f16x8* V4 = reinterpret_cast<const f16x8*>(args.V4);
+    {
+      const f16x8* p = K4 + (blk0 + keys[0]) * (kCap * D / 8);
 #pragma unroll
-      for (int s = 0; s < NS16; ++s) Qf[qt][s] = *reinterpret_cast<const f16x8*>(Qa + ((qt * NS16 + s) * 64 + lane) * 8);
-
+      for (int f = 0; f < 2 * NS16; ++f) dma_fragment(p + f * 64 + lane, sK + f * 64);
+    }
     for (int it = 0; it < n4; ++it) {
       const int kb = keys[it];
       const int nb = L.n_a[kb];
-      const _Float16* Kb = args.K4 + (blk0 + kb) * (int64_t)kCap * D;
-      const _Float16* Vb = args.V4 + (blk0 + kb) * (int64_t)kCap * D;
+      wait_vmem();  // key fragments of this block are in LDS
+      f16x8 kf[2][NS16];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int s = 0; s < NS16; ++s) kf[j][s] = sK[(j * NS16 + s) * 64 + lane];
+      f16x8 vf[NT][4];
+      {
+        const f16x8* p = V4 + (blk0 + kb) * (kCap * D / 8);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int s = 0; s < 4; ++s) vf[t][s] = p[(t * 4 + s) * 64 + lane];
+      }
       f32x16 S[2][2];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        S[0][j] = f32x16{};
-        S[1][j] = f32x16{};
+      for (int qt = 0; qt < 2; ++qt) S[qt][0] = S[qt][1] = f32x16{};
 #pragma unroll
-        for (int s = 0; s < NS16; ++s) {
-          const f16x8 kf = *reinterpret_cast<const f16x8*>(Kb + ((j * NS16 + s) * 64 + lane) * 8);
-          S[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, Qf[0][s], S[0][j], 0, 0, 0);
-          S[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, Qf[1][s], S[1][j], 0, 0, 0);
+      for (int s = 0; s < NS16; ++s) {
+        const f16x8 q0 = sQ[s * 64 + lane], q1 = sQ[(NS16 + s) * 64 + lane];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          S[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[j][s], q0, S[0][j], 0, 0, 0);
+          S[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[j][s], q1, S[1][j], 0, 0, 0);
         }
+      }
+      if (it + 1 < n4) {  // next block's keys stream into LDS during the softmax
+        wait_lds();
+        const f16x8* p = K4 + (blk0 + keys[it + 1]) * (kCap * D / 8);
+#pragma unroll
+        for (int f = 0; f < 2 * NS16; ++f) dma_fragment(p + f * 64 + lane, sK + f * 64);
+      }
+      if (nb < kCap) {  // partial key block: padded slots carry no weight
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              if (32 * j + 16 * g + i >= nb) S[qt][j][i] = -INFINITY;
       }
       f16x8 Pf[2][4];
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
-        float gm[2];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          if (nb < kCap) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i)
-              if (32 * j + 16 * g + i >= nb) S[qt][j][i] = -INFINITY;
-          }
-          float x = S[qt][j][0];
-#pragma unroll
-          for (int i = 1; i < 16; ++i) x = fmaxf(x, S[qt][j][i]);
-          gm[j] = x;
-        }
-        const float mn = update_max<NT>(fmaxf(gm[0], gm[1]), c4, m[qt], l[qt], U[qt]);
-        float lsum = 0.0f;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          // group maximum of Pt = exp2 of the group's maximum logit
-          const float pmax = exp2_fast(__builtin_fmaf(gm[j], c4, -mn));
-          const float sigma = e4m3_round_mag(448.0f * pmax);
-          const float rs = sigma == 0.0f ? 0.0f : __fdiv_rn(2688.0f, sigma);
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const float p = exp2_fast(__builtin_fmaf(S[qt][j][i], c4, -mn));
-            lsum += p;
-            Pf[qt][2 * j + (i >> 3)][i & 7] = (_Float16)(sigma * e2m1_round(p * rs));
-          }
-        }
-        l[qt] += lsum;
+        const float gm0 = max16(S[qt][0]), gm1 = max16(S[qt][1]);
+        const float mn = update_max<NT>(fmaxf(gm0, gm1), c4, m[qt], l[qt], U[qt]);
+        const float s0 = nvfp4_weights(S[qt][0], c4, mn, gm0, Pf[qt][0], Pf[qt][1]);
+        const float s1 = nvfp4_weights(S[qt][1], c4, mn, gm1, Pf[qt][2], Pf[qt][3]);
+        l[qt] += s0 + s1;
       }
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-          const f16x8 vf = *reinterpret_cast<const f16x8*>(Vb + ((t * 4 + s) * 64 + lane) * 8);
-          U[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, Pf[0][s], U[0][t], 0, 0, 0);
-          U[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf, Pf[1][s], U[1][t], 0, 0, 0);
+          U[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[t][s], Pf[0][s], U[0][t], 0, 0, 0);
+          U[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[t][s], Pf[1][s], U[1][t], 0, 0, 0);
         }
     }
   }
@@ -165,74 +240,94 @@ __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
     l[1] /= eta;
 
     i32x4 Qf[2][NS32];
-    const int8_t* Qa = args.Q8 + (blk0 + a) * (int64_t)kCap * D;
+    const i32x4* Qa = reinterpret_cast<const i32x4*>(args.Q8) + (blk0 + a) * (kCap * D / 16);
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-      for (int s = 0; s < NS32; ++s) Qf[qt][s] = *reinterpret_cast<const i32x4*>(Qa + ((qt * NS32 + s) * 64 + lane) * 16);
+      for (int s = 0; s < NS32; ++s) Qf[qt][s] = Qa[(qt * NS32 + s) * 64 + lane];
     const float c8a = args.dQ[blk0 + a] * kLog2e * rsqd;
-
+    const i32x4* K8 = reinterpret_cast<const i32x4*>(args.K8);
+    const i32x4* V8 = reinterpret_cast<const i32x4*>(args.V8);
+    i32x4* sK8 = reinterpret_cast<i32x4*>(sK);
+    wait_lds();
+    {
+      const i32x4* p = K8 + (blk0 + keys[n4]) * (kCap * D / 16);
+#pragma unroll
+      for (int f = 0; f < 2 * NS32; ++f) dma_fragment(p + f * 64 + lane, sK8 + f * 64);
+    }
     for (int it = 0; it < n8; ++it) {
       const int kb = keys[n4 + it];
       const int nb = L.n_a[kb];
       const float cb = c8a * args.dK[blk0 + kb];
-      const int8_t* Kb = args.K8 + (blk0 + kb) * (int64_t)kCap * D;
-      const uint8_t* Vb = args.V8 + (blk0 + kb) * (int64_t)kCap * D;
-      i32x16 S[2][2];
+      wait_vmem();  // key fragments of this block are in LDS
+      i32x4 kf[2][NS32];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        S[0][j] = i32x16{};
-        S[1][j] = i32x16{};
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int s = 0; s < NS32; ++s) {
-          const i32x4 kf = *reinterpret_cast<const i32x4*>(Kb + ((j * NS32 + s) * 64 + lane) * 16);
-          S[0][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf, Qf[0][s], S[0][j], 0, 0, 0);
-          S[1][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf, Qf[1][s], S[1][j], 0, 0, 0);
+        for (int s = 0; s < NS32; ++s) kf[j][s] = sK8[(j * NS32 + s) * 64 + lane];
+      i32x8 vf[NT];
+      {
+        const i32x4* p = V8 + (blk0 + kb) * (kCap * D / 16);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const i32x4 v0 = p[(t * 2 + 0) * 64 + lane], v1 = p[(t * 2 + 1) * 64 + lane];
+          vf[t] = i32x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
         }
       }
-      long Pf[2][4];
+      i32x16 S[2][2];
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) S[qt][0] = S[qt][1] = i32x16{};
+#pragma unroll
+      for (int s = 0; s < NS32; ++s)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          S[0][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf[j][s], Qf[0][s], S[0][j], 0, 0, 0);
+          S[1][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf[j][s], Qf[1][s], S[1][j], 0, 0, 0);
+        }
+      if (it + 1 < n8) {
+        wait_lds();
+        const i32x4* p = K8 + (blk0 + keys[n4 + it + 1]) * (kCap * D / 16);
+#pragma unroll
+        for (int f = 0; f < 2 * NS32; ++f) dma_fragment(p + f * 64 + lane, sK8 + f * 64);
+      }
+      i32x8 Pf[2];
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
-        float sf[2][16];
-        float bm = -INFINITY;
+        f32x16 sf[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            float v = (float)S[qt][j][i];
-            if (nb < kCap && 32 * j + 16 * g + i >= nb) v = -INFINITY;
-            sf[j][i] = v;
-            bm = fmaxf(bm, v);
-          }
-        const float mn = update_max<NT>(bm, cb, m[qt], l[qt], U[qt]);
+          for (int i = 0; i < 16; ++i) sf[j][i] = (float)S[qt][j][i];
+        if (nb < kCap) {
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              if (32 * j + 16 * g + i >= nb) sf[j][i] = -INFINITY;
+        }
+        const float mn = update_max<NT>(fmaxf(max16(sf[0]), max16(sf[1])), cb, m[qt], l[qt], U[qt]);
         const float off = kExpOffset - mn;
         float lsum = 0.0f;
 #pragma unroll
         for (int j = 0; j < 2; ++j)
 #pragma unroll
-          for (int h2 = 0; h2 < 2; ++h2) {
-            float p[8];
+          for (int w = 0; w < 4; ++w) {
+            float p[4];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              p[e] = exp2_fast(__builtin_fmaf(sf[j][8 * h2 + e], cb, off));
+            for (int e = 0; e < 4; ++e) {
+              p[e] = exp2_fast(__builtin_fmaf(sf[j][4 * w + e], cb, off));
               lsum += p[e];
             }
-            int lo = __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], 0, false);
-            lo = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], lo, true);
-            int hi = __builtin_amdgcn_cvt_pk_fp8_f32(p[4], p[5], 0, false);
-            hi = __builtin_amdgcn_cvt_pk_fp8_f32(p[6], p[7], hi, true);
-            Pf[qt][2 * j + h2] = (long)(((unsigned long)(unsigned)hi << 32) | (unsigned)lo);
+            int v = __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], 0, false);
+            Pf[qt][4 * j + w] = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], v, true);
           }
         l[qt] += lsum;
       }
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const long vf = *reinterpret_cast<const long*>(Vb + ((t * 2 + (s >> 1)) * 64 + lane) * 16 + 8 * (s & 1));
-          U[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(vf, Pf[0][s], U[0][t], 0, 0, 0);
-          U[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(vf, Pf[1][s], U[1][t], 0, 0, 0);
-        }
+      for (int t = 0; t < NT; ++t) {
+        U[0][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[t], Pf[0], U[0][t], 0, 0, 0, 127, 0, 127);
+        U[1][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[t], Pf[1], U[1][t], 0, 0, 0, 127, 0, 127);
+      }
     }
     // Exit: U_c <- eta delta_c U_c, l <- eta l
 #pragma unroll

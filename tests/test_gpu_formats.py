@@ -1,0 +1,102 @@
+"""Device format checks (gfx950): the library's software E4M3 / E2M1 encoders
+and the hardware conversion instructions used by the attention kernel, against
+the oracle's format definitions on exhaustive code tables, every midpoint
+(ties), neighbours of every midpoint and random values."""
+import ctypes
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import formats as F
+
+pytestmark = pytest.mark.gpu
+PROBE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "probes", "libda2_probe.so")
+
+
+def _values():
+    e4 = np.unique(np.abs(F.e4m3_decode(np.arange(0x7F))))
+    mids4 = (e4[:-1] + e4[1:]) / 2
+    e2 = F.E2M1_VALUES
+    mids2 = (e2[:-1] + e2[1:]) / 2
+    base = np.concatenate([e4, mids4, e2, mids2, [448.0, 449.0, 464.0, 470.0, 500.0, 1e6, 6.0, 6.5, 7.0, 100.0]])
+    base = base.astype(np.float32)
+    up = np.nextafter(base, np.float32(np.inf))
+    down = np.nextafter(base, np.float32(0))
+    rng = np.random.default_rng(0)
+    rand = np.concatenate([rng.uniform(0, 8, 20000), rng.uniform(0, 460, 20000),
+                           np.exp(rng.uniform(-25, 6, 20000))]).astype(np.float32)
+    x = np.concatenate([base, up, down, rand])
+    return np.concatenate([x, -x]).astype(np.float32)
+
+
+@pytest.fixture(scope="module")
+def probe():
+    assert torch.cuda.is_available()
+    lib = ctypes.CDLL(PROBE)
+    x = _values()
+    n = x.size
+    xd = torch.from_numpy(x).cuda()
+    outs = {k: torch.empty(n, dtype=dt, device="cuda") for k, dt in
+            [("e2m1_sw", torch.float32), ("e2m1_hw", torch.float32), ("e2m1_hw_s2", torch.float32),
+             ("e2m1_hw_back3", torch.float32), ("e4m3_sw", torch.int32), ("e4m3_hw", torch.int32),
+             ("e4m3_mag_sw", torch.float32)]}
+    order = ["e2m1_sw", "e2m1_hw", "e2m1_hw_s2", "e2m1_hw_back3", "e4m3_sw", "e4m3_hw", "e4m3_mag_sw"]
+    args = [ctypes.c_void_p(xd.data_ptr()), ctypes.c_int(n)] + [ctypes.c_void_p(outs[k].data_ptr()) for k in order]
+    args.append(ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert lib.da2_probe_formats(*args) == 0
+    torch.cuda.synchronize()
+    return x.astype(np.float64), {k: v.cpu().numpy() for k, v in outs.items()}
+
+
+def test_software_e2m1(probe):
+    x, o = probe
+    np.testing.assert_array_equal(o["e2m1_sw"], F.e2m1(x))
+
+
+def test_software_e4m3(probe):
+    x, o = probe
+    np.testing.assert_array_equal(o["e4m3_sw"].astype(np.uint8), F.e4m3_code(F.e4m3(x)))
+    np.testing.assert_array_equal(o["e4m3_mag_sw"], F.e4m3(np.abs(x)))
+
+
+def test_hardware_fp8_conversion_is_rne_in_range(probe):
+    """v_cvt_pk_fp8_f32 (used for the 8-bit path's weights, all in [0, 448])."""
+    x, o = probe
+    inr = np.abs(x) <= 448.0
+    want = F.e4m3_code(F.e4m3(x[inr]))
+    got = o["e4m3_hw"][inr].astype(np.uint8)
+    bad = np.nonzero(got != want)[0]
+    assert bad.size == 0, [(x[inr][i], got[i], want[i]) for i in bad[:10]]
+
+
+def test_hardware_fp4_conversion(probe):
+    """v_cvt_scalef32_pk_fp4_f32 then v_cvt_scalef32_pk_f16_fp4, unit scales:
+    round to nearest even with saturation, like the E2M1 cast definition."""
+    x, o = probe
+    want = F.e2m1(x)
+    bad = np.nonzero(o["e2m1_hw"] != want)[0]
+    print("fp4 hw mismatches:", bad.size, [(x[i], o["e2m1_hw"][i], want[i]) for i in bad[:12]])
+    # how the scale operands act (recorded for the kernel design)
+    s2_div = np.mean(o["e2m1_hw_s2"] == F.e2m1(x / 2))
+    s2_mul = np.mean(o["e2m1_hw_s2"] == F.e2m1(x * 2))
+    b3_full = np.mean(o["e2m1_hw_back3"] == F.e2m1(x) * 3)
+    b3_exp = np.mean(o["e2m1_hw_back3"] == F.e2m1(x) * 2)
+    print(f"encode scale 2: matches x/2 {s2_div:.4f}, x*2 {s2_mul:.4f}; "
+          f"decode scale 3: full {b3_full:.4f}, exponent only {b3_exp:.4f}")
+    assert bad.size == 0
+
+
+def test_lds_dma_placement():
+    """global_load_lds_dwordx4 puts lane i's 16 bytes at base + 16 i (the
+    attention kernel stages 1 KB operand fragments this way)."""
+    lib = ctypes.CDLL(PROBE)
+    src = torch.arange(256, dtype=torch.int32, device="cuda") * 7 + 3
+    out = torch.zeros(1024, dtype=torch.int32, device="cuda")
+    assert lib.da2_probe_lds_dma(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                 ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)) == 0
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert np.array_equal(o[64:320], src.cpu().numpy())
+    assert np.all(o[:64] == -1) and np.all(o[320:] == -1)
