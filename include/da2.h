@@ -135,7 +135,10 @@ int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num8, int3
  *              ascending in [0,n4), then its 8-bit key blocks ascending in
  *              [n4, n4+n8)
  *   [1] counts int32 [B*H*R][2] = (n4, n8)
- *   [2] order  int32 [B*H*R]: rows (b*H+h)*R+a, most expensive first
+ *   [2] order  int32 [B*H*R]: the work order of the rows (b*H+h)*R+a: grouped
+ *              by head and by row parity, most expensive first in each group;
+ *              attention workgroup w takes order[(w mod 8)*ceil(n/8) + w div 8]
+ *              (any permutation of the rows is a valid order)
  *   [3] meta   int32 [8]: [0] = number of rows in order                       */
 int32_t da2_lists_offsets(const da2_problem* p, int64_t* offsets4);
 

@@ -19,6 +19,7 @@ FLAGS = [
     "-ffp-contract=off",                          # encoders round every operation once
     "-fhip-fp32-correctly-rounded-divide-sqrt",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",         # keep MFMA accumulators in VGPRs (no AGPR copies)
     "-Wno-unused-command-line-argument",
 ]
 

@@ -56,17 +56,16 @@ __device__ inline void rescale(f32x16 (&U)[NT], float alpha) {
   for (int t = 0; t < NT; ++t) U[t] *= alpha;
 }
 
-// Running-max update for one 32-query tile: bm_in is this lane's maximum raw
-// logit of the block (-inf on padding), scale converts raw logits to log2 units.
-// Rescales l and U by 2^(m_old - m_new) and returns m_new.
-template <int NT>
-__device__ inline float update_max(float bm_in, float scale, float& m, float& l, f32x16 (&U)[NT]) {
-  const float bm = fmaxf(bm_in, __shfl_xor(bm_in, 32, 64));
+// Running-max update for one 32-query tile: bm_lane is this lane's maximum raw
+// logit of the block (-inf on padding), scale converts raw logits to log2
+// units. Updates m and l, returns the new maximum and (via alpha) the factor
+// 2^(m_old - m_new) that the numerator still has to be multiplied by.
+__device__ inline float new_max(float bm_lane, float scale, float& m, float& l, float& alpha) {
+  const float bm = fmaxf(bm_lane, __shfl_xor(bm_lane, 32, 64));
   const float mn = fmaxf(m, bm * scale);
-  const float alpha = exp2_fast(m - mn);
+  alpha = exp2_fast(m - mn);
   m = mn;
   l *= alpha;
-  if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
   return mn;
 }
 
@@ -77,32 +76,37 @@ __device__ inline float max16(const f32x16& v) {
   return fmaxf(fmaxf(fmaxf(a, b), fmaxf(c, d)), fmaxf(e, v[15]));
 }
 
+constexpr float kLog2_2688 = 11.392317422778760f;  // log2(6 * 448)
+
 // NVFP4 weights of one 16-slot group held by this lane (slots of S[0..15]):
 // sigma_P = E4M3(448 max Pt), w = sigma_P * E2M1(Pt * 2688 / sigma_P) as fp16
-// pairs for the P^T operand; returns the fp32 sum of Pt.
+// pairs for the P^T operand; returns the fp32 sum of Pt. The scaled weights
+// y = Pt * 2688 / sigma_P come from one exp2 each (the factor is folded into
+// the exponent); a zero sigma_P uses factor 1, and those y (all below 2^-18)
+// round to E2M1 zero as the format requires.
 __device__ inline float nvfp4_weights(const f32x16& S, float c, float mn, float gmax, f16x8& lo, f16x8& hi) {
   const float pmax = exp2_fast(__builtin_fmaf(gmax, c, -mn));
   const float sigma = e4m3_round_mag(fminf(448.0f * pmax, 448.0f));
-  const float rs = sigma > 0.0f ? 2688.0f * __builtin_amdgcn_rcpf(sigma) : 0.0f;
+  const bool nz = sigma > 0.0f;
+  const float off = (nz ? kLog2_2688 - __builtin_amdgcn_logf(sigma) : 0.0f) - mn;
   const _Float16 sh = (_Float16)sigma;
   const f16x2 s2 = {sh, sh};
-  float p[16];
+  float y[16];
   float sum = 0.0f;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    p[i] = exp2_fast(__builtin_fmaf(S[i], c, -mn));
-    sum += p[i];
-    p[i] *= rs;
+    y[i] = exp2_fast(__builtin_fmaf(S[i], c, off));
+    sum += y[i];
   }
   // E2M1 codes, two per byte (byte selector must be a literal)
-  uint32_t f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, p[0], p[1], 1.0f, 0);
-  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, p[2], p[3], 1.0f, 1);
-  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, p[4], p[5], 1.0f, 2);
-  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, p[6], p[7], 1.0f, 3);
-  uint32_t f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, p[8], p[9], 1.0f, 0);
-  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, p[10], p[11], 1.0f, 1);
-  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, p[12], p[13], 1.0f, 2);
-  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, p[14], p[15], 1.0f, 3);
+  uint32_t f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
+  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, y[2], y[3], 1.0f, 1);
+  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, y[4], y[5], 1.0f, 2);
+  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, y[6], y[7], 1.0f, 3);
+  uint32_t f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[8], y[9], 1.0f, 0);
+  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[10], y[11], 1.0f, 1);
+  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[12], y[13], 1.0f, 2);
+  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[14], y[15], 1.0f, 3);
   // back to fp16 and times sigma_P (exact: at most 6 significant bits)
   const f16x2 a0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 0) * s2;
   const f16x2 a1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 1) * s2;
@@ -114,23 +118,113 @@ __device__ inline float nvfp4_weights(const f32x16& S, float c, float mn, float 
   const f16x2 b3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f1, 1.0f, 3) * s2;
   lo = f16x8{a0[0], a0[1], a1[0], a1[1], a2[0], a2[1], a3[0], a3[1]};
   hi = f16x8{b0[0], b0[1], b1[0], b1[1], b2[0], b2[1], b3[0], b3[1]};
-  return sum;
+  return sum * (nz ? sigma * (1.0f / 2688.0f) : 1.0f);
+}
+
+// Padded key slots (slot >= nb) of a partial block get -inf logits.
+__device__ inline void mask_tail(f32x16 (&S)[2], int nb, int g) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (32 * j + 16 * g + i >= nb) S[j][i] = -INFINITY;
+}
+
+// Key-list window: lane i holds entry first+i of the row's list of key blocks
+// (block id, valid slots, INT8 key scale), so each iteration reads its entry
+// with one readlane instead of a chain of dependent global loads.
+struct KeyWin {
+  int kb, nb;
+  float dk;
+};
+__device__ inline KeyWin key_window(const uint16_t* list, int first, int count, const int32_t* n_a,
+                                    const float* dK, int lane) {
+  KeyWin w{0, kCap, 0.0f};
+  const int e = first + lane;
+  if (e < count) {
+    w.kb = list[e];
+    w.nb = n_a[w.kb];
+    w.dk = dK[w.kb];
+  }
+  return w;
+}
+__device__ inline int lane_value(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
+__device__ inline float lane_value(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// Interleave hint for the scheduler: n rounds of one MFMA followed by k VALU
+// instructions, so the matrix and vector pipes work at the same time.
+template <int N, int K>
+__device__ inline void interleave_mfma_valu() {
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, K, 0);
+  }
+}
+
+// Softmax of one 32-query tile on the NVFP4 path: running max, NVFP4 weights,
+// denominator; returns the numerator's rescale factor through alpha.
+__device__ inline void softmax_fp4(f32x16 (&S)[2], int nb, int g, float c4, float& m, float& l, float& alpha,
+                                   f16x8 (&Pf)[4]) {
+  if (nb < kCap) mask_tail(S, nb, g);
+  const float gm0 = max16(S[0]), gm1 = max16(S[1]);
+  const float mn = new_max(fmaxf(gm0, gm1), c4, m, l, alpha);
+  const float s0 = nvfp4_weights(S[0], c4, mn, gm0, Pf[0], Pf[1]);
+  const float s1 = nvfp4_weights(S[1], c4, mn, gm1, Pf[2], Pf[3]);
+  l += s0 + s1;
+}
+
+// Softmax of one 32-query tile on the INT8 path: amplified weights
+// 2^((s - m) log2 e + 8.807) in E4M3 for the fp8 P^T operand.
+__device__ inline void softmax_fp8(const i32x16 (&Si)[2], int nb, int g, float cb, float& m, float& l, float& alpha,
+                                   i32x8& Pf) {
+  f32x16 sf[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sf[j][i] = (float)Si[j][i];
+  if (nb < kCap) mask_tail(sf, nb, g);
+  const float mn = new_max(fmaxf(max16(sf[0]), max16(sf[1])), cb, m, l, alpha);
+  const float off = kExpOffset - mn;
+  float lsum = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      float p[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        p[e] = exp2_fast(__builtin_fmaf(sf[j][4 * w + e], cb, off));
+        lsum += p[e];
+      }
+      const int v = __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], 0, false);
+      Pf[4 * j + w] = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], v, true);
+    }
+  l += lsum;
 }
 
 template <int D>
 __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
   constexpr int NS16 = D / 16, NS32 = D / 32, NT = D / 32;
   __shared__ f16x8 sQ[2 * NS16 * 64];  // query fragments of the current phase (16 KB at d=128)
-  __shared__ f16x8 sK[2 * NS16 * 64];  // key fragments of the next block (DMA target)
+  __shared__ f16x8 sK[2 * NS16 * 64];  // key fragments of the current block (DMA target)
   const int lane = threadIdx.x, r = lane & 31, g = lane >> 5;
   const int R = args.R;
-  const int item = args.order[blockIdx.x];
-  if (item < 0) return;
+  // XCD-aware mapping: workgroup b runs on XCD b mod 8 and takes the next row
+  // of that XCD's contiguous segment of the work order.
+  const int n_items = args.B * args.H * R;
+  const int seg = (n_items + 7) >> 3;
+  const int idx = (int)(blockIdx.x & 7) * seg + (int)(blockIdx.x >> 3);
+  if (idx >= n_items) return;
+  const int item = args.order[idx];
   const int bh = item / R, a = item % R;
   const Layout L = layout_view(args.layout, R, args.Npad);
   const int n4 = args.counts[2 * item], n8 = args.counts[2 * item + 1];
   const uint16_t* keys = args.keys + (int64_t)item * R;
   const int64_t blk0 = (int64_t)bh * R;  // first block of this head
+  const float* dKh = args.dK + blk0;
   const float rsqd = 1.0f / sqrtf((float)D);
 
   f32x16 U[2][NT];
@@ -147,73 +241,72 @@ __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
     const f16x8* Qa = reinterpret_cast<const f16x8*>(args.Q4) + (blk0 + a) * (kCap * D / 8);
 #pragma unroll
     for (int c = 0; c < 2 * NS16; ++c) sQ[c * 64 + lane] = Qa[c * 64 + lane];
-    const f16x8* K4 = reinterpret_cast<const f16x8*>(args.K4);
-    const f16x8* V4 = reinterpret_cast<const f16x8*>(args.V4);
+    const f16x8* K4 = reinterpret_cast<const f16x8*>(args.K4) + blk0 * (kCap * D / 8);
+    const f16x8* V4 = reinterpret_cast<const f16x8*>(args.V4) + blk0 * (kCap * D / 8);
+    KeyWin win = key_window(keys, 0, n4, L.n_a, dKh, lane);
+    KeyWin nxt = key_window(keys, 64, n4, L.n_a, dKh, lane);
     {
-      const f16x8* p = K4 + (blk0 + keys[0]) * (kCap * D / 8);
+      const f16x8* p = K4 + lane_value(win.kb, 0) * (kCap * D / 8);
 #pragma unroll
       for (int f = 0; f < 2 * NS16; ++f) dma_fragment(p + f * 64 + lane, sK + f * 64);
     }
     for (int it = 0; it < n4; ++it) {
-      const int kb = keys[it];
-      const int nb = L.n_a[kb];
+      const int sl = it & 63;
+      if (sl == 0 && it > 0) {
+        win = nxt;
+        nxt = key_window(keys, it + 64, n4, L.n_a, dKh, lane);
+      }
+      const int kb = lane_value(win.kb, sl);
+      const int nb = lane_value(win.nb, sl);
+      const int kb_next = sl < 63 ? lane_value(win.kb, sl + 1) : lane_value(nxt.kb, 0);
       wait_vmem();  // key fragments of this block are in LDS
-      f16x8 kf[2][NS16];
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int s = 0; s < NS16; ++s) kf[j][s] = sK[(j * NS16 + s) * 64 + lane];
       f16x8 vf[NT][4];
       {
-        const f16x8* p = V4 + (blk0 + kb) * (kCap * D / 8);
+        const f16x8* p = V4 + kb * (kCap * D / 8);
 #pragma unroll
         for (int t = 0; t < NT; ++t)
 #pragma unroll
           for (int s = 0; s < 4; ++s) vf[t][s] = p[(t * 4 + s) * 64 + lane];
       }
-      f32x16 S[2][2];
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt) S[qt][0] = S[qt][1] = f32x16{};
+      f32x16 S0[2] = {f32x16{}, f32x16{}}, S1[2] = {f32x16{}, f32x16{}};
 #pragma unroll
       for (int s = 0; s < NS16; ++s) {
-        const f16x8 q0 = sQ[s * 64 + lane], q1 = sQ[(NS16 + s) * 64 + lane];
+        const f16x8 q0 = sQ[s * 64 + lane];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          S[0][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[j][s], q0, S[0][j], 0, 0, 0);
-          S[1][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf[j][s], q1, S[1][j], 0, 0, 0);
-        }
+        for (int j = 0; j < 2; ++j)
+          S0[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sK[(j * NS16 + s) * 64 + lane], q0, S0[j], 0, 0, 0);
       }
-      if (it + 1 < n4) {  // next block's keys stream into LDS during the softmax
+      // query tile 1's QK^T runs on the matrix pipe while tile 0's softmax runs
+#pragma unroll
+      for (int s = 0; s < NS16; ++s) {
+        const f16x8 q1 = sQ[(NS16 + s) * 64 + lane];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          S1[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sK[(j * NS16 + s) * 64 + lane], q1, S1[j], 0, 0, 0);
+      }
+      float alpha0, alpha1;
+      f16x8 P0[4], P1[4];
+      softmax_fp4(S0, nb, g, c4, m[0], l[0], alpha0, P0);
+      interleave_mfma_valu<2 * NS16, 18>();
+      if (it + 1 < n4) {  // next block's keys stream into LDS during the rest of this block
         wait_lds();
-        const f16x8* p = K4 + (blk0 + keys[it + 1]) * (kCap * D / 8);
+        const f16x8* p = K4 + kb_next * (kCap * D / 8);
 #pragma unroll
         for (int f = 0; f < 2 * NS16; ++f) dma_fragment(p + f * 64 + lane, sK + f * 64);
       }
-      if (nb < kCap) {  // partial key block: padded slots carry no weight
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int i = 0; i < 16; ++i)
-              if (32 * j + 16 * g + i >= nb) S[qt][j][i] = -INFINITY;
-      }
-      f16x8 Pf[2][4];
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        const float gm0 = max16(S[qt][0]), gm1 = max16(S[qt][1]);
-        const float mn = update_max<NT>(fmaxf(gm0, gm1), c4, m[qt], l[qt], U[qt]);
-        const float s0 = nvfp4_weights(S[qt][0], c4, mn, gm0, Pf[qt][0], Pf[qt][1]);
-        const float s1 = nvfp4_weights(S[qt][1], c4, mn, gm1, Pf[qt][2], Pf[qt][3]);
-        l[qt] += s0 + s1;
-      }
+      if (__ballot(alpha0 != 1.0f)) rescale<NT>(U[0], alpha0);
+      // tile 0's P^T V product runs on the matrix pipe while tile 1's softmax runs
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          U[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[t][s], Pf[0][s], U[0][t], 0, 0, 0);
-          U[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[t][s], Pf[1][s], U[1][t], 0, 0, 0);
-        }
+        for (int s = 0; s < 4; ++s) U[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[t][s], P0[s], U[0][t], 0, 0, 0);
+      softmax_fp4(S1, nb, g, c4, m[1], l[1], alpha1, P1);
+      interleave_mfma_valu<4 * NT, 18>();
+      if (__ballot(alpha1 != 1.0f)) rescale<NT>(U[1], alpha1);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) U[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[t][s], P1[s], U[1][t], 0, 0, 0);
     }
   }
 
@@ -246,88 +339,69 @@ __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
 #pragma unroll
       for (int s = 0; s < NS32; ++s) Qf[qt][s] = Qa[(qt * NS32 + s) * 64 + lane];
     const float c8a = args.dQ[blk0 + a] * kLog2e * rsqd;
-    const i32x4* K8 = reinterpret_cast<const i32x4*>(args.K8);
-    const i32x4* V8 = reinterpret_cast<const i32x4*>(args.V8);
+    const i32x4* K8 = reinterpret_cast<const i32x4*>(args.K8) + blk0 * (kCap * D / 16);
+    const i32x4* V8 = reinterpret_cast<const i32x4*>(args.V8) + blk0 * (kCap * D / 16);
     i32x4* sK8 = reinterpret_cast<i32x4*>(sK);
+    const uint16_t* keys8 = keys + n4;
+    KeyWin win = key_window(keys8, 0, n8, L.n_a, dKh, lane);
+    KeyWin nxt = key_window(keys8, 64, n8, L.n_a, dKh, lane);
     wait_lds();
     {
-      const i32x4* p = K8 + (blk0 + keys[n4]) * (kCap * D / 16);
+      const i32x4* p = K8 + lane_value(win.kb, 0) * (kCap * D / 16);
 #pragma unroll
       for (int f = 0; f < 2 * NS32; ++f) dma_fragment(p + f * 64 + lane, sK8 + f * 64);
     }
     for (int it = 0; it < n8; ++it) {
-      const int kb = keys[n4 + it];
-      const int nb = L.n_a[kb];
-      const float cb = c8a * args.dK[blk0 + kb];
+      const int sl = it & 63;
+      if (sl == 0 && it > 0) {
+        win = nxt;
+        nxt = key_window(keys8, it + 64, n8, L.n_a, dKh, lane);
+      }
+      const int kb = lane_value(win.kb, sl);
+      const int nb = lane_value(win.nb, sl);
+      const float cb = c8a * lane_value(win.dk, sl);
+      const int kb_next = sl < 63 ? lane_value(win.kb, sl + 1) : lane_value(nxt.kb, 0);
       wait_vmem();  // key fragments of this block are in LDS
-      i32x4 kf[2][NS32];
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int s = 0; s < NS32; ++s) kf[j][s] = sK8[(j * NS32 + s) * 64 + lane];
       i32x8 vf[NT];
       {
-        const i32x4* p = V8 + (blk0 + kb) * (kCap * D / 16);
+        const i32x4* p = V8 + kb * (kCap * D / 16);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
           const i32x4 v0 = p[(t * 2 + 0) * 64 + lane], v1 = p[(t * 2 + 1) * 64 + lane];
           vf[t] = i32x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
         }
       }
-      i32x16 S[2][2];
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt) S[qt][0] = S[qt][1] = i32x16{};
+      i32x16 S0[2] = {i32x16{}, i32x16{}}, S1[2] = {i32x16{}, i32x16{}};
 #pragma unroll
       for (int s = 0; s < NS32; ++s)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          S[0][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf[j][s], Qf[0][s], S[0][j], 0, 0, 0);
-          S[1][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(kf[j][s], Qf[1][s], S[1][j], 0, 0, 0);
-        }
+        for (int j = 0; j < 2; ++j)
+          S0[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(sK8[(j * NS32 + s) * 64 + lane], Qf[0][s], S0[j], 0, 0, 0);
+#pragma unroll
+      for (int s = 0; s < NS32; ++s)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          S1[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(sK8[(j * NS32 + s) * 64 + lane], Qf[1][s], S1[j], 0, 0, 0);
+      float alpha0, alpha1;
+      i32x8 P0, P1;
+      softmax_fp8(S0, nb, g, cb, m[0], l[0], alpha0, P0);
+      interleave_mfma_valu<2 * NS32, 20>();
       if (it + 1 < n8) {
         wait_lds();
-        const i32x4* p = K8 + (blk0 + keys[n4 + it + 1]) * (kCap * D / 16);
+        const i32x4* p = K8 + kb_next * (kCap * D / 16);
 #pragma unroll
         for (int f = 0; f < 2 * NS32; ++f) dma_fragment(p + f * 64 + lane, sK8 + f * 64);
       }
-      i32x8 Pf[2];
+      if (__ballot(alpha0 != 1.0f)) rescale<NT>(U[0], alpha0);
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-        f32x16 sf[2];
+      for (int t = 0; t < NT; ++t)
+        U[0][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[t], P0, U[0][t], 0, 0, 0, 127, 0, 127);
+      softmax_fp8(S1, nb, g, cb, m[1], l[1], alpha1, P1);
+      interleave_mfma_valu<NT, 40>();
+      if (__ballot(alpha1 != 1.0f)) rescale<NT>(U[1], alpha1);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) sf[j][i] = (float)S[qt][j][i];
-        if (nb < kCap) {
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int i = 0; i < 16; ++i)
-              if (32 * j + 16 * g + i >= nb) sf[j][i] = -INFINITY;
-        }
-        const float mn = update_max<NT>(fmaxf(max16(sf[0]), max16(sf[1])), cb, m[qt], l[qt], U[qt]);
-        const float off = kExpOffset - mn;
-        float lsum = 0.0f;
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            float p[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              p[e] = exp2_fast(__builtin_fmaf(sf[j][4 * w + e], cb, off));
-              lsum += p[e];
-            }
-            int v = __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], 0, false);
-            Pf[qt][4 * j + w] = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], v, true);
-          }
-        l[qt] += lsum;
-      }
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        U[0][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[t], Pf[0], U[0][t], 0, 0, 0, 127, 0, 127);
-        U[1][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[t], Pf[1], U[1][t], 0, 0, 0, 127, 0, 127);
-      }
+      for (int t = 0; t < NT; ++t)
+        U[1][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[t], P1, U[1][t], 0, 0, 0, 127, 0, 127);
     }
     // Exit: U_c <- eta delta_c U_c, l <- eta l
 #pragma unroll
@@ -379,10 +453,11 @@ __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
 
 hipError_t launch_attn(const AttnArgs& args, hipStream_t stream) {
   const int items = args.B * args.H * args.R;
+  const int grid = 8 * ((items + 7) / 8);
   if (args.d == 128)
-    hipLaunchKernelGGL(mixed_attn_kernel<128>, dim3(items), dim3(64), 0, stream, args);
+    hipLaunchKernelGGL(mixed_attn_kernel<128>, dim3(grid), dim3(64), 0, stream, args);
   else
-    hipLaunchKernelGGL(mixed_attn_kernel<64>, dim3(items), dim3(64), 0, stream, args);
+    hipLaunchKernelGGL(mixed_attn_kernel<64>, dim3(grid), dim3(64), 0, stream, args);
   return hipGetLastError();
 }
 

@@ -46,13 +46,15 @@ __device__ inline float load_elem(const void* base, int64_t idx, int dtype) {
 
 // ---- E4M3 ------------------------------------------------------------------
 // Value of a >= 0 after a round-to-nearest-even cast to E4M3 (saturating).
+// Branch-free: both the subnormal (step 2^-9) and the normal rounding are
+// evaluated and selected.
 __device__ inline float e4m3_round_mag(float a) {
-  if (!(a < 448.0f)) return 448.0f;
-  if (a < 0.015625f) return __builtin_rintf(a * 512.0f) * 0.001953125f;  // subnormals, step 2^-9
+  const float sub = __builtin_rintf(a * 512.0f) * 0.001953125f;
   uint32_t b = __float_as_uint(a);
   b += 0x7FFFFu + ((b >> 20) & 1u);
   b &= 0xFFF00000u;
-  return fminf(__uint_as_float(b), 448.0f);
+  const float nrm = __uint_as_float(b);
+  return fminf(a < 0.015625f ? sub : nrm, 448.0f);
 }
 
 // Byte code of x after a round-to-nearest-even, saturating cast to E4M3.

@@ -201,19 +201,33 @@ __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
   }
 }
 
-// One workgroup: counting sort of rows by cost, most expensive first.
+// One workgroup: counting sort of the rows into the attention work order.
+// Rows are grouped by head and, inside a head, by row parity (two half-heads
+// with near-equal cost); each group is sorted most expensive first. The
+// attention launch hands workgroup b the entry (b mod 8) * ceil(n/8) + b div 8,
+// and workgroups are dispatched round-robin over the 8 XCDs, so each XCD walks
+// one contiguous segment (about n/8 rows of one or two heads, whose K/V then
+// share that XCD's L2) longest-first.
 constexpr int kOrderBins = 8192;
+__device__ inline int order_key(const RankArgs& args, int64_t i) {
+  const int BH = args.B * args.H;
+  const int64_t cmax = 5ll * args.R;
+  const int groups = 2 * BH;
+  const int nbh = groups < kOrderBins ? kOrderBins / groups : 1;  // cost bins per group
+  const int bh = (int)(i / args.R), half = (int)(i % args.R) & 1;
+  const int bin = (int)((int64_t)args.cost[i] * (nbh - 1) / (cmax > 0 ? cmax : 1));
+  int64_t key = (int64_t)(2 * bh + half) * nbh + (nbh - 1 - bin);
+  if ((int64_t)groups * nbh > kOrderBins) key = key * kOrderBins / ((int64_t)groups * nbh);
+  return (int)key;
+}
+
 __global__ __launch_bounds__(1024) void rank_order_kernel(RankArgs args) {
   __shared__ uint32_t hist[kOrderBins];
   __shared__ uint32_t part[1024];
   const int64_t n = (int64_t)args.B * args.H * args.R;
-  const int64_t cmax = 5ll * args.R;
   for (int i = threadIdx.x; i < kOrderBins; i += 1024) hist[i] = 0u;
   __syncthreads();
-  for (int64_t i = threadIdx.x; i < n; i += 1024) {
-    const int bin = (int)((int64_t)args.cost[i] * (kOrderBins - 1) / (cmax > 0 ? cmax : 1));
-    atomicAdd(&hist[kOrderBins - 1 - bin], 1u);  // descending cost -> ascending bin
-  }
+  for (int64_t i = threadIdx.x; i < n; i += 1024) atomicAdd(&hist[order_key(args, i)], 1u);
   __syncthreads();
   constexpr int per = kOrderBins / 1024;
   uint32_t s = 0;
@@ -237,8 +251,7 @@ __global__ __launch_bounds__(1024) void rank_order_kernel(RankArgs args) {
   }
   __syncthreads();
   for (int64_t i = threadIdx.x; i < n; i += 1024) {
-    const int bin = (int)((int64_t)args.cost[i] * (kOrderBins - 1) / (cmax > 0 ? cmax : 1));
-    const uint32_t pos = atomicAdd(&hist[kOrderBins - 1 - bin], 1u);
+    const uint32_t pos = atomicAdd(&hist[order_key(args, i)], 1u);
     args.order[pos] = (int32_t)i;
   }
   if (threadIdx.x == 0) args.meta[0] = (int32_t)n;
