@@ -43,9 +43,14 @@ __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
 // Asynchronous copy of one 1 KB operand fragment (16 bytes per lane, lane
-// order) from global memory to LDS at the wave-uniform address dst.
+// order) from global memory to LDS at the wave-uniform address dst. Issued as
+// inline assembly so that the compiler does not add its conservative
+// "wait for every LDS copy" before later LDS reads; the kernel waits for
+// exactly the copies it needs (wait_vmem_keep) instead.
 __device__ inline void dma_fragment(const void* src_lane, void* dst) {
-  __builtin_amdgcn_global_load_lds(src_lane, (lds_ptr)dst, 16, 0, 0);
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr)dst)));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src_lane), "s"(lds)
+               : "memory", "m0");
 }
 __device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 __device__ inline void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
@@ -146,6 +151,9 @@ __device__ inline KeyWin key_window(const uint16_t* list, int first, int count, 
     w.nb = n_a[w.kb];
     w.dk = dK[w.kb];
   }
+  // Consume the loaded registers here, so the wait for these loads happens in
+  // the (rare) refill and not at every later use of the window.
+  asm volatile("" : "+v"(w.kb), "+v"(w.nb), "+v"(w.dk));
   return w;
 }
 __device__ inline int lane_value(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
@@ -153,19 +161,26 @@ __device__ inline float lane_value(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// Interleave hint for the scheduler: n rounds of one MFMA followed by k VALU
-// instructions, so the matrix and vector pipes work at the same time.
-template <int N, int K>
-__device__ inline void interleave_mfma_valu() {
-#pragma unroll
-  for (int i = 0; i < N; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, K, 0);
-  }
+// Waits for this wave's older vector-memory operations, leaving the N most
+// recent ones in flight (they complete in issue order).
+template <int N>
+__device__ inline void wait_vmem_keep() {
+  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (N == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else static_assert(N == 0, "unsupported count");
+}
+// Workgroup barrier without the memory fences of __syncthreads (the waits
+// above make LDS contents ready; the fences would also drain in-flight DMA).
+__device__ inline void wg_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
-// Softmax of one 32-query tile on the NVFP4 path: running max, NVFP4 weights,
-// denominator; returns the numerator's rescale factor through alpha.
+// Softmax of this wave's 32-query tile on the NVFP4 path: running max, NVFP4
+// weights, denominator; the numerator's rescale factor comes back in alpha.
 __device__ inline void softmax_fp4(f32x16 (&S)[2], int nb, int g, float c4, float& m, float& l, float& alpha,
                                    f16x8 (&Pf)[4]) {
   if (nb < kCap) mask_tail(S, nb, g);
@@ -176,7 +191,7 @@ __device__ inline void softmax_fp4(f32x16 (&S)[2], int nb, int g, float c4, floa
   l += s0 + s1;
 }
 
-// Softmax of one 32-query tile on the INT8 path: amplified weights
+// Softmax of this wave's 32-query tile on the INT8 path: amplified weights
 // 2^((s - m) log2 e + 8.807) in E4M3 for the fp8 P^T operand.
 __device__ inline void softmax_fp8(const i32x16 (&Si)[2], int nb, int g, float cb, float& m, float& l, float& alpha,
                                    i32x8& Pf) {
@@ -205,12 +220,69 @@ __device__ inline void softmax_fp8(const i32x16 (&Si)[2], int nb, int g, float c
   l += lsum;
 }
 
+// One precision phase of the block loop. The workgroup's two waves own the
+// query tiles qt = 0, 1 of the block; the key and value tiles of each key
+// block are copied into LDS once (each wave issues half of the fragments) and
+// read by both waves. Per block i:
+//   wait K(i) -> barrier -> S = K Q^T -> barrier -> DMA K(i+1)
+//   softmax (overlaps the K(i+1) and V(i) copies)
+//   wait V(i) -> barrier -> U += V^T P^T -> barrier -> DMA V(i+1)
+// Frag: fragment type; NFK/NFV: fragments per K/V tile.
+// Orders a wait after the computation of v (an empty use of the register).
+template <typename T>
+__device__ inline void after(const T& v) {
+  asm volatile("" ::"v"(v));
+}
+
+template <int NFK, int NFV, typename Frag, typename QK, typename SM, typename PV>
+__device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_a, const float* dKh,
+                                  const Frag* Kh, const Frag* Vh, Frag* sK, Frag* sV, int wave, int lane,
+                                  QK qk, SM softmax, PV pv) {
+  constexpr int TILE = NFK * 64;  // fragments per block, in Frag units (K and V have the same size)
+  static_assert(NFK == NFV, "K and V tiles hold the same number of fragments");
+  constexpr int HALF = NFK / 2;
+  auto dma_tile = [&](const Frag* src, Frag* dst) {
+#pragma unroll
+    for (int f = wave * HALF; f < (wave + 1) * HALF; ++f) dma_fragment(src + f * 64 + lane, dst + f * 64);
+  };
+  KeyWin win = key_window(list, 0, n, n_a, dKh, lane);
+  dma_tile(Kh + (int64_t)lane_value(win.kb, 0) * TILE, sK);
+  dma_tile(Vh + (int64_t)lane_value(win.kb, 0) * TILE, sV);
+  for (int it = 0; it < n; ++it) {
+    const int sl = it & 63;
+    if (sl == 0 && it > 0) win = key_window(list, it, n, n_a, dKh, lane);
+    const int kb = lane_value(win.kb, sl);
+    const int nb = lane_value(win.nb, sl);
+    const float dk = lane_value(win.dk, sl);
+    const bool more = it + 1 < n;
+    const int kb_next = !more ? 0 : (sl < 63 ? lane_value(win.kb, sl + 1) : (int)list[it + 1]);
+    wait_vmem_keep<HALF>();  // K(i) copied (V(i), issued later, may still be in flight)
+    wg_barrier();
+    qk(nb, dk);
+    wait_lds();
+    wg_barrier();  // both waves are done with sK
+    if (more) dma_tile(Kh + (int64_t)kb_next * TILE, sK);
+    softmax(nb, dk);  // returns after its results exist, so the wait below cannot move above it
+    if (more)
+      wait_vmem_keep<HALF>();  // V(i) copied, K(i+1) may still be in flight
+    else
+      wait_vmem_keep<0>();
+    wg_barrier();
+    pv();
+    wait_lds();
+    wg_barrier();  // both waves are done with sV
+    if (more) dma_tile(Vh + (int64_t)kb_next * TILE, sV);
+    (void)kb;
+  }
+}
+
 template <int D>
-__global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
+__global__ __launch_bounds__(128) void mixed_attn_kernel(AttnArgs args) {
   constexpr int NS16 = D / 16, NS32 = D / 32, NT = D / 32;
-  __shared__ f16x8 sQ[2 * NS16 * 64];  // query fragments of the current phase (16 KB at d=128)
-  __shared__ f16x8 sK[2 * NS16 * 64];  // key fragments of the current block (DMA target)
-  const int lane = threadIdx.x, r = lane & 31, g = lane >> 5;
+  __shared__ f16x8 sK[2 * NS16 * 64];  // key tile of the current block (16 KB at d=128)
+  __shared__ f16x8 sV[NT * 4 * 64];    // value tile of the current block
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r = lane & 31, g = lane >> 5;
+  const int qt = wave;  // this wave's 32-query tile
   const int R = args.R;
   // XCD-aware mapping: workgroup b runs on XCD b mod 8 and takes the next row
   // of that XCD's contiguous segment of the work order.
@@ -227,87 +299,45 @@ __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
   const float* dKh = args.dK + blk0;
   const float rsqd = 1.0f / sqrtf((float)D);
 
-  f32x16 U[2][NT];
+  f32x16 U[NT];
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-    for (int t = 0; t < NT; ++t) U[qt][t] = f32x16{};
-  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.0f, 0.0f};
+  for (int t = 0; t < NT; ++t) U[t] = f32x16{};
+  float m = -INFINITY, l = 0.0f;
   const float gV = args.g[bh * 4 + 2];
 
   // ------------------------------ NVFP4 phase ------------------------------
   if (n4 > 0) {
     const float c4 = args.g[bh * 4 + 0] * args.g[bh * 4 + 1] * kLog2e * rsqd;
+    f16x8 Qf[NS16];
     const f16x8* Qa = reinterpret_cast<const f16x8*>(args.Q4) + (blk0 + a) * (kCap * D / 8);
 #pragma unroll
-    for (int c = 0; c < 2 * NS16; ++c) sQ[c * 64 + lane] = Qa[c * 64 + lane];
-    const f16x8* K4 = reinterpret_cast<const f16x8*>(args.K4) + blk0 * (kCap * D / 8);
-    const f16x8* V4 = reinterpret_cast<const f16x8*>(args.V4) + blk0 * (kCap * D / 8);
-    KeyWin win = key_window(keys, 0, n4, L.n_a, dKh, lane);
-    KeyWin nxt = key_window(keys, 64, n4, L.n_a, dKh, lane);
-    {
-      const f16x8* p = K4 + lane_value(win.kb, 0) * (kCap * D / 8);
+    for (int s = 0; s < NS16; ++s) Qf[s] = Qa[(qt * NS16 + s) * 64 + lane];
+    f32x16 S[2];
+    f16x8 P[4];
+    float alpha = 1.0f;
+    auto qk = [&](int, float) {
+      S[0] = S[1] = f32x16{};
 #pragma unroll
-      for (int f = 0; f < 2 * NS16; ++f) dma_fragment(p + f * 64 + lane, sK + f * 64);
-    }
-    for (int it = 0; it < n4; ++it) {
-      const int sl = it & 63;
-      if (sl == 0 && it > 0) {
-        win = nxt;
-        nxt = key_window(keys, it + 64, n4, L.n_a, dKh, lane);
-      }
-      const int kb = lane_value(win.kb, sl);
-      const int nb = lane_value(win.nb, sl);
-      const int kb_next = sl < 63 ? lane_value(win.kb, sl + 1) : lane_value(nxt.kb, 0);
-      wait_vmem();  // key fragments of this block are in LDS
-      f16x8 vf[NT][4];
-      {
-        const f16x8* p = V4 + kb * (kCap * D / 8);
+      for (int s = 0; s < NS16; ++s)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          S[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sK[(j * NS16 + s) * 64 + lane], Qf[s], S[j], 0, 0, 0);
+    };
+    auto sm = [&](int nb, float) {
+      softmax_fp4(S, nb, g, c4, m, l, alpha, P);
+      after(P[0]), after(P[1]), after(P[2]), after(P[3]), after(l);
+    };
+    auto pv = [&]() {
+      if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-#pragma unroll
-          for (int s = 0; s < 4; ++s) vf[t][s] = p[(t * 4 + s) * 64 + lane];
-      }
-      f32x16 S0[2] = {f32x16{}, f32x16{}}, S1[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-      for (int s = 0; s < NS16; ++s) {
-        const f16x8 q0 = sQ[s * 64 + lane];
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          S0[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sK[(j * NS16 + s) * 64 + lane], q0, S0[j], 0, 0, 0);
-      }
-      // query tile 1's QK^T runs on the matrix pipe while tile 0's softmax runs
-#pragma unroll
-      for (int s = 0; s < NS16; ++s) {
-        const f16x8 q1 = sQ[(NS16 + s) * 64 + lane];
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          S1[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sK[(j * NS16 + s) * 64 + lane], q1, S1[j], 0, 0, 0);
-      }
-      float alpha0, alpha1;
-      f16x8 P0[4], P1[4];
-      softmax_fp4(S0, nb, g, c4, m[0], l[0], alpha0, P0);
-      interleave_mfma_valu<2 * NS16, 18>();
-      if (it + 1 < n4) {  // next block's keys stream into LDS during the rest of this block
-        wait_lds();
-        const f16x8* p = K4 + kb_next * (kCap * D / 8);
-#pragma unroll
-        for (int f = 0; f < 2 * NS16; ++f) dma_fragment(p + f * 64 + lane, sK + f * 64);
-      }
-      if (__ballot(alpha0 != 1.0f)) rescale<NT>(U[0], alpha0);
-      // tile 0's P^T V product runs on the matrix pipe while tile 1's softmax runs
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int s = 0; s < 4; ++s) U[0][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[t][s], P0[s], U[0][t], 0, 0, 0);
-      softmax_fp4(S1, nb, g, c4, m[1], l[1], alpha1, P1);
-      interleave_mfma_valu<4 * NT, 18>();
-      if (__ballot(alpha1 != 1.0f)) rescale<NT>(U[1], alpha1);
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int s = 0; s < 4; ++s) U[1][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(vf[t][s], P1[s], U[1][t], 0, 0, 0);
-    }
+          U[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sV[(t * 4 + s) * 64 + lane], P[s], U[t], 0, 0, 0);
+    };
+    phase_loop<2 * NS16, NT * 4>(keys, n4, L.n_a, dKh, reinterpret_cast<const f16x8*>(args.K4) + blk0 * (kCap * D / 8),
+                                 reinterpret_cast<const f16x8*>(args.V4) + blk0 * (kCap * D / 8), sK, sV, wave, lane,
+                                 qk, sm, pv);
   }
 
   // per-lane channel of accumulator register i of channel tile t
@@ -325,139 +355,93 @@ __global__ __launch_bounds__(64) void mixed_attn_kernel(AttnArgs args) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const float dc = dV[chan(t, i)];
-        const float f = dc == 0.0f ? 0.0f : restore / (eta * dc);
-        U[0][t][i] *= f;
-        U[1][t][i] *= f;
+        U[t][i] *= dc == 0.0f ? 0.0f : restore / (eta * dc);
       }
-    l[0] /= eta;
-    l[1] /= eta;
-
-    i32x4 Qf[2][NS32];
+    l /= eta;
+    i32x4 Qf[NS32];
     const i32x4* Qa = reinterpret_cast<const i32x4*>(args.Q8) + (blk0 + a) * (kCap * D / 16);
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-      for (int s = 0; s < NS32; ++s) Qf[qt][s] = Qa[(qt * NS32 + s) * 64 + lane];
+    for (int s = 0; s < NS32; ++s) Qf[s] = Qa[(qt * NS32 + s) * 64 + lane];
     const float c8a = args.dQ[blk0 + a] * kLog2e * rsqd;
-    const i32x4* K8 = reinterpret_cast<const i32x4*>(args.K8) + blk0 * (kCap * D / 16);
-    const i32x4* V8 = reinterpret_cast<const i32x4*>(args.V8) + blk0 * (kCap * D / 16);
     i32x4* sK8 = reinterpret_cast<i32x4*>(sK);
-    const uint16_t* keys8 = keys + n4;
-    KeyWin win = key_window(keys8, 0, n8, L.n_a, dKh, lane);
-    KeyWin nxt = key_window(keys8, 64, n8, L.n_a, dKh, lane);
+    i32x4* sV8 = reinterpret_cast<i32x4*>(sV);
+    i32x16 S[2];
+    i32x8 P;
+    float alpha = 1.0f;
+    auto qk = [&](int, float) {
+      S[0] = S[1] = i32x16{};
+#pragma unroll
+      for (int s = 0; s < NS32; ++s)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          S[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(sK8[(j * NS32 + s) * 64 + lane], Qf[s], S[j], 0, 0, 0);
+    };
+    auto sm = [&](int nb, float dk) {
+      softmax_fp8(S, nb, g, c8a * dk, m, l, alpha, P);
+      after(P), after(l);
+    };
+    auto pv = [&]() {
+      if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const i32x4 v0 = sV8[(t * 2 + 0) * 64 + lane], v1 = sV8[(t * 2 + 1) * 64 + lane];
+        const i32x8 vf = i32x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+        U[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf, P, U[t], 0, 0, 0, 127, 0, 127);
+      }
+    };
     wait_lds();
-    {
-      const i32x4* p = K8 + lane_value(win.kb, 0) * (kCap * D / 16);
-#pragma unroll
-      for (int f = 0; f < 2 * NS32; ++f) dma_fragment(p + f * 64 + lane, sK8 + f * 64);
-    }
-    for (int it = 0; it < n8; ++it) {
-      const int sl = it & 63;
-      if (sl == 0 && it > 0) {
-        win = nxt;
-        nxt = key_window(keys8, it + 64, n8, L.n_a, dKh, lane);
-      }
-      const int kb = lane_value(win.kb, sl);
-      const int nb = lane_value(win.nb, sl);
-      const float cb = c8a * lane_value(win.dk, sl);
-      const int kb_next = sl < 63 ? lane_value(win.kb, sl + 1) : lane_value(nxt.kb, 0);
-      wait_vmem();  // key fragments of this block are in LDS
-      i32x8 vf[NT];
-      {
-        const i32x4* p = V8 + kb * (kCap * D / 16);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          const i32x4 v0 = p[(t * 2 + 0) * 64 + lane], v1 = p[(t * 2 + 1) * 64 + lane];
-          vf[t] = i32x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-        }
-      }
-      i32x16 S0[2] = {i32x16{}, i32x16{}}, S1[2] = {i32x16{}, i32x16{}};
-#pragma unroll
-      for (int s = 0; s < NS32; ++s)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          S0[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(sK8[(j * NS32 + s) * 64 + lane], Qf[0][s], S0[j], 0, 0, 0);
-#pragma unroll
-      for (int s = 0; s < NS32; ++s)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          S1[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(sK8[(j * NS32 + s) * 64 + lane], Qf[1][s], S1[j], 0, 0, 0);
-      float alpha0, alpha1;
-      i32x8 P0, P1;
-      softmax_fp8(S0, nb, g, cb, m[0], l[0], alpha0, P0);
-      interleave_mfma_valu<2 * NS32, 20>();
-      if (it + 1 < n8) {
-        wait_lds();
-        const i32x4* p = K8 + kb_next * (kCap * D / 16);
-#pragma unroll
-        for (int f = 0; f < 2 * NS32; ++f) dma_fragment(p + f * 64 + lane, sK8 + f * 64);
-      }
-      if (__ballot(alpha0 != 1.0f)) rescale<NT>(U[0], alpha0);
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-        U[0][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[t], P0, U[0][t], 0, 0, 0, 127, 0, 127);
-      softmax_fp8(S1, nb, g, cb, m[1], l[1], alpha1, P1);
-      interleave_mfma_valu<NT, 40>();
-      if (__ballot(alpha1 != 1.0f)) rescale<NT>(U[1], alpha1);
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-        U[1][t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf[t], P1, U[1][t], 0, 0, 0, 127, 0, 127);
-    }
+    wg_barrier();  // the NVFP4 phase is done with sK / sV
+    phase_loop<2 * NS32, NT * 2>(keys + n4, n8, L.n_a, dKh,
+                                 reinterpret_cast<const i32x4*>(args.K8) + blk0 * (kCap * D / 16),
+                                 reinterpret_cast<const i32x4*>(args.V8) + blk0 * (kCap * D / 16), sK8, sV8, wave,
+                                 lane, qk, sm, pv);
     // Exit: U_c <- eta delta_c U_c, l <- eta l
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float f = eta * dV[chan(t, i)];
-        U[0][t][i] *= f;
-        U[1][t][i] *= f;
-      }
-    l[0] *= eta;
-    l[1] *= eta;
+      for (int i = 0; i < 16; ++i) U[t][i] *= eta * dV[chan(t, i)];
+    l *= eta;
   } else if (n4 > 0) {
     const float restore = gV / 2688.0f;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      U[0][t] *= restore;
-      U[1][t] *= restore;
-    }
+    for (int t = 0; t < NT; ++t) U[t] *= restore;
   }
 
   // ------------------------- normalize and scatter -------------------------
   const int nq = L.n_a[a];
   const int32_t* s2t = L.slot2tok + (int64_t)a * kCap;
   const int b = bh / args.H, h = bh % args.H;
+  const float lt = l + __shfl_xor(l, 32, 64);
+  const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
+  const int q = 32 * qt + r;
+  if (q < nq) {
+    const int64_t row = (int64_t)b * args.ob + (int64_t)h * args.oh + (int64_t)s2t[q] * args.on;
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
-    const float lt = l[qt] + __shfl_xor(l[qt], 32, 64);
-    const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
-    const int q = 32 * qt + r;
-    if (q < nq) {
-      const int64_t row = (int64_t)b * args.ob + (int64_t)h * args.oh + (int64_t)s2t[q] * args.on;
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float v = U[qt][t][i] * inv;
-          if (args.odtype == DA2_FP32) {
-            reinterpret_cast<float*>(args.O)[row + chan(t, i)] = v;
-          } else {
-            const uint32_t u = __float_as_uint(v);
-            const uint32_t rb = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-            reinterpret_cast<uint16_t*>(args.O)[row + chan(t, i)] = static_cast<uint16_t>(rb);
-          }
+      for (int i = 0; i < 16; ++i) {
+        const float v = U[t][i] * inv;
+        if (args.odtype == DA2_FP32) {
+          reinterpret_cast<float*>(args.O)[row + chan(t, i)] = v;
+        } else {
+          const uint32_t u = __float_as_uint(v);
+          const uint32_t rb = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+          reinterpret_cast<uint16_t*>(args.O)[row + chan(t, i)] = static_cast<uint16_t>(rb);
         }
-    }
+      }
   }
 }
+
+template __global__ void mixed_attn_kernel<64>(AttnArgs);
+template __global__ void mixed_attn_kernel<128>(AttnArgs);
 
 hipError_t launch_attn(const AttnArgs& args, hipStream_t stream) {
   const int items = args.B * args.H * args.R;
   const int grid = 8 * ((items + 7) / 8);
   if (args.d == 128)
-    hipLaunchKernelGGL(mixed_attn_kernel<128>, dim3(grid), dim3(64), 0, stream, args);
+    hipLaunchKernelGGL(mixed_attn_kernel<128>, dim3(grid), dim3(128), 0, stream, args);
   else
-    hipLaunchKernelGGL(mixed_attn_kernel<64>, dim3(grid), dim3(64), 0, stream, args);
+    hipLaunchKernelGGL(mixed_attn_kernel<64>, dim3(grid), dim3(128), 0, stream, args);
   return hipGetLastError();
 }
 
