@@ -58,7 +58,10 @@ typedef struct {
   int32_t B, H, d, T, Hg, Wg;
 } da2_problem;
 
-/* A [B, H, N, d] tensor with d contiguous; strides are in elements. */
+/* A [B, H, N, d] tensor with d contiguous; strides are in elements. Input
+ * tensors (Q, K, V) are read in 16-byte vectors: their base pointers must be
+ * 16-byte aligned and every stride a multiple of 16 bytes (8 bf16 or 4 fp32
+ * elements), else the call returns DA2_ERR_INVALID_ARG. */
 typedef struct {
   int64_t stride_b, stride_h, stride_n;
   int32_t dtype; /* da2_dtype */

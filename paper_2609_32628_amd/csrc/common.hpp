@@ -44,6 +44,25 @@ __device__ inline float load_elem(const void* base, int64_t idx, int dtype) {
   return reinterpret_cast<const float*>(base)[idx];
 }
 
+// 16-byte vector load of consecutive channels at p (16-byte aligned) as floats:
+// 8 bf16 or 4 fp32 values.
+__device__ inline void load_chunk(const uint16_t* p, float* x) {
+  const uint4 v = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+__device__ inline void load_chunk(const float* p, float* x) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  x[0] = v.x;
+  x[1] = v.y;
+  x[2] = v.z;
+  x[3] = v.w;
+}
+
 // ---- E4M3 ------------------------------------------------------------------
 // Value of a >= 0 after a round-to-nearest-even cast to E4M3 (saturating).
 // Branch-free: both the subnormal (step 2^-9) and the normal rounding are

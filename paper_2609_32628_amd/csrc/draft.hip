@@ -1,7 +1,7 @@
 // Draft map kernels (descriptor equation; Definition 3.1).
 //
-//   draft_pool     one workgroup per (block, head): mean (float64 sum / n_a) and
-//                  channel max over the valid tokens of Q and K, plus the per-head
+//   draft_pool     one workgroup per (block, head, Q or K): mean (float64 sum /
+//                  n_a) and channel max over the valid tokens, plus the per-head
 //                  max|Q|, max|K| used by the NVFP4 tensor scales.
 //   draft_logits   64x64 tiles of Qbar Kbar^T / sqrt d and Qmax Kmax^T / sqrt d in
 //                  float64, both operands staged through LDS in 16-channel slices.
@@ -18,53 +18,79 @@ __global__ void zero_u32_kernel(uint32_t* p, int64_t stride, int count, int64_t 
   (void)n_rows;
 }
 
-template <int D>
+// One workgroup per (block, head, Q or K). Thread (row group rg, chunk cc)
+// reads 16-byte chunks of the block's valid slots rg, rg + RG, ...; the
+// per-channel float64 sums and float32 maxima are reduced across row groups
+// (lanes CPR apart, then the four waves through LDS).
+template <int D, typename T>
 __global__ __launch_bounds__(256) void draft_pool_kernel(DraftArgs args) {
-  constexpr int G = 256 / D;  // token groups
-  __shared__ double s_sum[G][D];
-  __shared__ float s_max[G][D];
-  __shared__ float s_amax[8];
-  const int a = blockIdx.x, bh = blockIdx.y;
-  const int b = bh / args.H, h = bh % args.H;
+  constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte load
+  constexpr int CPR = D / EPC;         // loads per slot row
+  constexpr int RG = 256 / CPR;        // row groups
+  constexpr int RPT = kCap / RG;       // rows per thread
+  __shared__ double s_sum[4][D];
+  __shared__ float s_max[4][D];
+  __shared__ float s_amax[4];
+  const int a = blockIdx.x, bh = blockIdx.y, which = blockIdx.z;
+  const int b = bh / args.H, h = bh % args.H, tid = threadIdx.x;
   const Layout L = layout_view(args.layout, args.R, args.Npad);
   const int n = L.n_a[a];
   const int32_t* slots = L.slot2tok + (int64_t)a * kCap;
-  const int c = threadIdx.x % D, grp = threadIdx.x / D;
-  for (int which = 0; which < 2; ++which) {
-    const void* X = which == 0 ? args.Q : args.K;
-    const int64_t base = (int64_t)b * args.sb + (int64_t)h * args.sh;
-    double sum = 0.0;
-    float mx = -INFINITY, amax = 0.0f;
-    for (int i = grp; i < n; i += G) {
-      float x = load_elem(X, base + (int64_t)slots[i] * args.sn + c, args.dtype);
-      sum += (double)x;
-      mx = fmaxf(mx, x);
-      amax = fmaxf(amax, fabsf(x));
-    }
-    s_sum[grp][c] = sum;
-    s_max[grp][c] = mx;
-    float w = wave_max(amax);
-    if ((threadIdx.x & 63) == 0) s_amax[threadIdx.x >> 6] = w;
-    __syncthreads();
-    if (threadIdx.x < D) {
-      double t = 0.0;
-      float m = -INFINITY;
-      for (int q = 0; q < G; ++q) {
-        t += s_sum[q][c];
-        m = fmaxf(m, s_max[q][c]);
+  const int cc = tid % CPR, rg = tid / CPR;
+  const T* X = static_cast<const T*>(which == 0 ? args.Q : args.K) + (int64_t)b * args.sb + (int64_t)h * args.sh +
+               cc * EPC;
+  float x[RPT][EPC];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int s = rg + RG * k;
+    if (s < n) load_chunk(X + (int64_t)slots[s] * args.sn, x[k]);
+  }
+  double sum[EPC];
+  float mx[EPC];
+  float amax = 0.0f;
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) {
+    sum[e] = 0.0;
+    mx[e] = -INFINITY;
+  }
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    if (rg + RG * k < n) {
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        sum[e] += (double)x[k][e];
+        mx[e] = fmaxf(mx[e], x[k][e]);
+        amax = fmaxf(amax, fabsf(x[k][e]));
       }
-      const int64_t o = ((int64_t)bh * args.R + a) * D + c;
-      double* mean_out = which == 0 ? args.Qbar : args.Kbar;
-      double* max_out = which == 0 ? args.Qmax : args.Kmax;
-      mean_out[o] = t / (double)n;
-      max_out[o] = (double)m;
     }
-    if (threadIdx.x == 0) {
-      float m = s_amax[0];
-      for (int q = 1; q < 4; ++q) m = fmaxf(m, s_amax[q]);
-      atomic_max_pos(args.stats + (int64_t)bh * (4 + D) + which, m);
+  }
+#pragma unroll
+  for (int o = CPR; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+      sum[e] += __shfl_xor(sum[e], o, 64);
+      mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], o, 64));
     }
-    __syncthreads();
+  const int w = tid >> 6, lane = tid & 63;
+  if (lane < CPR)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) {
+      s_sum[w][cc * EPC + e] = sum[e];
+      s_max[w][cc * EPC + e] = mx[e];
+    }
+  amax = wave_max(amax);
+  if (lane == 0) s_amax[w] = amax;
+  __syncthreads();
+  if (tid < D) {
+    const double t = (s_sum[0][tid] + s_sum[1][tid]) + (s_sum[2][tid] + s_sum[3][tid]);
+    const float m = fmaxf(fmaxf(s_max[0][tid], s_max[1][tid]), fmaxf(s_max[2][tid], s_max[3][tid]));
+    const int64_t o = ((int64_t)bh * args.R + a) * D + tid;
+    (which == 0 ? args.Qbar : args.Kbar)[o] = t / (double)n;
+    (which == 0 ? args.Qmax : args.Kmax)[o] = (double)m;
+  }
+  if (tid == 0) {
+    const float m = fmaxf(fmaxf(s_amax[0], s_amax[1]), fmaxf(s_amax[2], s_amax[3]));
+    atomic_max_pos(args.stats + (int64_t)bh * (4 + D) + which, m);
   }
 }
 
@@ -159,10 +185,18 @@ hipError_t launch_draft(const DraftArgs& args, hipStream_t stream) {
   const int BH = args.B * args.H;
   hipLaunchKernelGGL(zero_u32_kernel, dim3(BH), dim3(64), 0, stream, args.stats, (int64_t)(4 + args.d), 2,
                      (int64_t)BH);
-  if (args.d == 128)
-    hipLaunchKernelGGL(draft_pool_kernel<128>, dim3(args.R, BH), dim3(256), 0, stream, args);
-  else
-    hipLaunchKernelGGL(draft_pool_kernel<64>, dim3(args.R, BH), dim3(256), 0, stream, args);
+  const dim3 pool_grid(args.R, BH, 2);
+  if (args.d == 128) {
+    if (args.dtype == DA2_BF16)
+      hipLaunchKernelGGL((draft_pool_kernel<128, uint16_t>), pool_grid, dim3(256), 0, stream, args);
+    else
+      hipLaunchKernelGGL((draft_pool_kernel<128, float>), pool_grid, dim3(256), 0, stream, args);
+  } else {
+    if (args.dtype == DA2_BF16)
+      hipLaunchKernelGGL((draft_pool_kernel<64, uint16_t>), pool_grid, dim3(256), 0, stream, args);
+    else
+      hipLaunchKernelGGL((draft_pool_kernel<64, float>), pool_grid, dim3(256), 0, stream, args);
+  }
   const int nt = (args.R + 63) / 64;
   hipLaunchKernelGGL(draft_logits_kernel, dim3(nt, nt, BH), dim3(256), 0, stream, args);
   hipLaunchKernelGGL(draft_softmax_kernel, dim3(args.R, BH), dim3(256), 0, stream, args);

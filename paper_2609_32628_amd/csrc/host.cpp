@@ -87,9 +87,14 @@ int32_t check_tensor(const da2_tensor* t, const Dims& d, bool out) {
   if (t->dtype != DA2_BF16 && t->dtype != DA2_FP32) return DA2_ERR_INVALID_ARG;
   if (t->stride_b <= 0 || t->stride_h <= 0 || t->stride_n <= 0) return DA2_ERR_INVALID_ARG;
   if (t->stride_n < d.d) return DA2_ERR_INVALID_ARG;
-  (void)out;
+  if (!out) {  // inputs are read in 16-byte vectors
+    const int64_t per = t->dtype == DA2_BF16 ? 8 : 4;
+    if (t->stride_b % per || t->stride_h % per || t->stride_n % per) return DA2_ERR_INVALID_ARG;
+  }
   return DA2_OK;
 }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // gfx950 check, cached per device ordinal (0 unknown, 1 ok, 2 unsupported).
 std::atomic<int8_t> g_arch_ok[64];
@@ -198,6 +203,7 @@ int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const 
   if (st) return st;
   if ((st = check_tensor(qk, d, false))) return st;
   if (!Q || !K || !layout || !A || !stats || !ws) return DA2_ERR_INVALID_ARG;
+  if (!aligned16(Q) || !aligned16(K)) return DA2_ERR_INVALID_ARG;
   if (!(lambda >= 0.0 && lambda <= 1.0)) return DA2_ERR_INVALID_ARG;
   da2_sizes_t sz;
   sizes_of(d, DA2_SCOPE_HEAD, &sz);
@@ -286,6 +292,7 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
   if (st) return st;
   if ((st = check_tensor(qkv, d, false))) return st;
   if (!Q || !K || !V || !layout || !stats || !ops) return DA2_ERR_INVALID_ARG;
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V)) return DA2_ERR_INVALID_ARG;
   (void)ws;
   if (ws_bytes < 0) return DA2_ERR_WORKSPACE;
   if ((st = check_device())) return st;
@@ -305,6 +312,7 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
   a.d = (int)d.d;
   a.R = (int)d.R;
   a.Npad = (int)d.Npad;
+  a.N = (int)d.N;
   a.layout = layout;
   a.stats = static_cast<uint32_t*>(stats);
   a.Q4 = reinterpret_cast<_Float16*>(ob + off[0]);

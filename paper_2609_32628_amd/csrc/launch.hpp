@@ -44,7 +44,7 @@ struct PrepArgs {
   const void* V;
   int64_t sb, sh, sn;
   int dtype;
-  int B, H, d, R, Npad;
+  int B, H, d, R, Npad, N;
   const int32_t* layout;
   uint32_t* stats;
   // ops sections

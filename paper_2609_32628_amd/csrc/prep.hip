@@ -1,17 +1,25 @@
 // Operand preparation kernels (format appendix; NVFP4 quantization equation).
 //
-//   prep_vstats   per (b,h,channel) max|V| over valid keys and per-head max|V|.
-//   prep_encode   one workgroup per (block, head): stages the 64-slot tile of Q,
-//                 K and V in LDS (gathered through slot2tok, padding = 0) and
-//                 writes every encoding in the MFMA fragment order of the
-//                 attention kernel (16-byte chunks, one per lane of a fragment):
-//                   INT8 Q, K with per-block scales,
-//                   E4M3 V with per-channel scales,
-//                   NVFP4 Q, K (16-channel groups) and V (16-slot groups) as the
-//                   exact fp16 value sigma*e.
+//   prep_vstats  token-major pass over V of each head: per-channel max|V| and
+//                the head's max|V| (every token is a valid key).
+//   prep_qk      one workgroup per (block, head, Q or K): gathers the block's
+//                64 slots through slot2tok in 16-byte loads (padding = 0);
+//                each thread owns whole 16-channel groups, so the INT8 block
+//                code and the NVFP4 group code of a group come from registers.
+//   prep_v       one workgroup per (block, head): the V tile is staged in LDS
+//                and read transposed, each thread owning one channel pair and
+//                one 16-slot group (the NVFP4 group of V runs along slots).
+// Every encoding is written in the MFMA fragment order of the attention kernel
+// (16-byte chunks, one per lane of a fragment):
+//   INT8 Q, K with per-block scales, E4M3 V with per-channel scales,
+//   NVFP4 Q, K (16-channel groups) and V (16-slot groups) as the exact fp16
+//   value sigma*e.
 // Scale arithmetic is float32 with one rounding per operation in the documented
 // order (the build uses -ffp-contract=off); division by a scale is a
-// multiplication by its correctly rounded float32 reciprocal.
+// multiplication by its correctly rounded float32 reciprocal. The E2M1 and E4M3
+// casts of scaled values use the gfx950 conversion instructions (round to
+// nearest even, saturating, signed zeros kept; checked by the device format
+// tests).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -22,30 +30,65 @@ __global__ void zero_vstats_kernel(uint32_t* stats, int d) {
   for (int i = 2 + threadIdx.x; i < 4 + d; i += blockDim.x) s[i] = 0u;
 }
 
-template <int D>
+// ---- V statistics -----------------------------------------------------------
+constexpr int kVstatRows = 256;  // tokens per workgroup
+
+template <int D, typename T>
 __global__ __launch_bounds__(256) void prep_vstats_kernel(PrepArgs args) {
-  constexpr int G = 256 / D;
-  __shared__ float s_max[G][D];
-  const int a = blockIdx.x, bh = blockIdx.y;
-  const int b = bh / args.H, h = bh % args.H;
-  const Layout L = layout_view(args.layout, args.R, args.Npad);
-  const int n = L.n_a[a];
-  const int32_t* slots = L.slot2tok + (int64_t)a * kCap;
-  const int c = threadIdx.x % D, grp = threadIdx.x / D;
-  const int64_t base = (int64_t)b * args.sb + (int64_t)h * args.sh;
-  float m = 0.0f;
-  for (int i = grp; i < n; i += G) m = fmaxf(m, fabsf(load_elem(args.V, base + (int64_t)slots[i] * args.sn + c, args.dtype)));
-  s_max[grp][c] = m;
+  constexpr int EPC = 16 / sizeof(T);   // elements per 16-byte load
+  constexpr int CPR = D / EPC;          // loads per token row
+  constexpr int RG = 256 / CPR;         // row groups
+  constexpr int RPT = kVstatRows / RG;  // rows per thread
+  __shared__ float s_max[4][D];
+  __shared__ float s_all[4];
+  const int bh = blockIdx.y, b = bh / args.H, h = bh % args.H, tid = threadIdx.x;
+  const int cc = tid % CPR, rg = tid / CPR;
+  const int t0 = blockIdx.x * kVstatRows;
+  const T* X = static_cast<const T*>(args.V) + (int64_t)b * args.sb + (int64_t)h * args.sh + cc * EPC;
+  float x[RPT][EPC];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int t = t0 + rg + RG * k;
+    if (t < args.N) {
+      load_chunk(X + (int64_t)t * args.sn, x[k]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) x[k][e] = 0.0f;
+    }
+  }
+  float m[EPC];
+#pragma unroll
+  for (int e = 0; e < EPC; ++e) {
+    m[e] = fabsf(x[0][e]);
+#pragma unroll
+    for (int k = 1; k < RPT; ++k) m[e] = fmaxf(m[e], fabsf(x[k][e]));
+  }
+  // lanes with the same chunk column sit CPR apart in a wave
+#pragma unroll
+  for (int o = CPR; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) m[e] = fmaxf(m[e], __shfl_xor(m[e], o, 64));
+  const int w = tid >> 6, lane = tid & 63;
+  if (lane < CPR)
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) s_max[w][cc * EPC + e] = m[e];
   __syncthreads();
-  if (threadIdx.x < D) {
-    float t = s_max[0][c];
-    for (int q = 1; q < G; ++q) t = fmaxf(t, s_max[q][c]);
+  if (tid < D) {
+    const float t = fmaxf(fmaxf(s_max[0][tid], s_max[1][tid]), fmaxf(s_max[2][tid], s_max[3][tid]));
     uint32_t* st = args.stats + (int64_t)bh * (4 + D);
-    atomic_max_pos(st + 4 + c, t);
-    atomic_max_pos(st + 2, t);
+    atomic_max_pos(st + 4 + tid, t);
+    const float wm = wave_max(t);
+    if ((tid & 63) == 0) s_all[tid >> 6] = wm;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float t = s_all[0];
+    for (int q = 1; q < D / 64; ++q) t = fmaxf(t, s_all[q]);
+    atomic_max_pos(args.stats + (int64_t)bh * (4 + D) + 2, t);
   }
 }
 
+// ---- shared encoders ------------------------------------------------------------
 // Row (slot) of MFMA A-operand row r of key tile j: puts the 16-slot group
 // 32j+16g+[0,16) of a query row into lane group g of the 32x32 accumulator.
 __device__ inline int kappa(int j, int r) { return 32 * j + 16 * ((r >> 2) & 1) + 4 * (r >> 3) + (r & 3); }
@@ -55,147 +98,225 @@ __device__ inline float nvfp4_scale_global(uint32_t amax_bits) {
   return g == 0.0f ? 1.0f : g;
 }
 
-template <int D>
-__global__ __launch_bounds__(256) void prep_encode_kernel(PrepArgs args) {
-  constexpr int LD = D + 1;
-  constexpr int NS16 = D / 16, NS32 = D / 32;
-  __shared__ float tile[kCap * LD];
+// INT8 codes of 16 values: round half away from zero of f32(x * inv), clamped.
+__device__ inline uint4 int8_codes16(const float* x, float inv) {
+  uint32_t w[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t packed = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float v = fminf(fmaxf(roundf(__fmul_rn(x[4 * q + e], inv)), -127.0f), 127.0f);
+      packed |= (static_cast<uint32_t>(static_cast<int>(v)) & 0xFFu) << (8 * e);
+    }
+    w[q] = packed;
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// sigma * E2M1(y) for 8 scaled values y, as fp16 (exact; an E2M1 zero keeps
+// the sign of y, as the hardware cast does).
+__device__ inline uint4 nvfp4_values8(const float* y, f16x2 s2) {
+  uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[2], y[3], 1.0f, 1);
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[4], y[5], 1.0f, 2);
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[6], y[7], 1.0f, 3);
+  const f16x2 d0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 0) * s2;
+  const f16x2 d1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 1) * s2;
+  const f16x2 d2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 2) * s2;
+  const f16x2 d3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 3) * s2;
+  return make_uint4(__builtin_bit_cast(uint32_t, d0), __builtin_bit_cast(uint32_t, d1),
+                    __builtin_bit_cast(uint32_t, d2), __builtin_bit_cast(uint32_t, d3));
+}
+
+// NVFP4 encoding of one 16-element group x with tensor scale gX (sixg = f32(6 gX)):
+// the two fp16 chunks of elements [0,8) and [8,16).
+__device__ inline void nvfp4_group16(const float* x, float gX, float sixg, uint4& lo, uint4& hi) {
+  float gm = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) gm = fmaxf(gm, fabsf(x[e]));
+  const float sigma = e4m3_round_mag(__fdiv_rn(gm, sixg));
+  if (sigma == 0.0f) {
+    lo = hi = make_uint4(0u, 0u, 0u, 0u);
+    return;
+  }
+  const float inv = __fdiv_rn(1.0f, __fmul_rn(gX, sigma));
+  float y[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) y[e] = __fmul_rn(x[e], inv);
+  const _Float16 sh = (_Float16)sigma;
+  const f16x2 s2 = {sh, sh};
+  lo = nvfp4_values8(y, s2);
+  hi = nvfp4_values8(y + 8, s2);
+}
+
+// ---- Q and K ----------------------------------------------------------------
+template <int D, typename T>
+__global__ __launch_bounds__(256) void prep_qk_kernel(PrepArgs args) {
+  constexpr int EPC = 16 / sizeof(T);
+  constexpr int NG = D / 16;                // 16-channel groups per slot
+  constexpr int UPT = kCap * NG / 256;      // groups per thread
+  constexpr int NS32 = D / 32;
   __shared__ float s_red[4];
-  __shared__ float s_invc[D];  // E4M3 V: f32(1/delta_c) (0 for a zero channel)
-  const int a = blockIdx.x, bh = blockIdx.y;
-  const int b = bh / args.H, h = bh % args.H;
-  const int R = args.R;
+  const int a = blockIdx.x, bh = blockIdx.y, which = blockIdx.z;  // which: 0 = Q, 1 = K
+  const int b = bh / args.H, h = bh % args.H, R = args.R, tid = threadIdx.x;
   const Layout L = layout_view(args.layout, R, args.Npad);
   const int n = L.n_a[a];
   const int32_t* slots = L.slot2tok + (int64_t)a * kCap;
-  const int64_t base = (int64_t)b * args.sb + (int64_t)h * args.sh;
-  const uint32_t* st = args.stats + (int64_t)bh * (4 + D);
-  const int64_t blk = (int64_t)bh * R + a;  // block index in [B*H*R]
-  const int tid = threadIdx.x;
+  const T* X = static_cast<const T*>(which == 0 ? args.Q : args.K) + (int64_t)b * args.sb + (int64_t)h * args.sh;
+  const int64_t blk = (int64_t)bh * R + a;
 
-  for (int which = 0; which < 3; ++which) {
-    const void* X = which == 0 ? args.Q : (which == 1 ? args.K : args.V);
-    // ---- stage the tile (slot order, padding 0) and its abs max ----
-    float amax = 0.0f;
-    for (int e = tid; e < kCap * D; e += 256) {
-      const int s = e / D, c = e % D;
-      float x = 0.0f;
-      if (s < n) x = load_elem(X, base + (int64_t)slots[s] * args.sn + c, args.dtype);
-      tile[s * LD + c] = x;
-      amax = fmaxf(amax, fabsf(x));
-    }
-    amax = wave_max(amax);
-    if ((tid & 63) == 0) s_red[tid >> 6] = amax;
-    if (which == 2 && tid < D) {
-      const float dlt = __fdiv_rn(__uint_as_float(st[4 + tid]), 2.25f);
-      s_invc[tid] = dlt == 0.0f ? 0.0f : __fdiv_rn(1.0f, dlt);
-    }
-    __syncthreads();
-    const float gX = nvfp4_scale_global(st[which]);
-    const float sixg = __fmul_rn(6.0f, gX);
-
-    if (which < 2) {
-      // ---- INT8, per-block scale ----
-      const float bmax = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
-      const float delta = __fadd_rn(__fdiv_rn(bmax, 127.0f), 1e-7f);
-      const float inv = __fdiv_rn(1.0f, delta);
-      if (tid == 0) (which == 0 ? args.dQ : args.dK)[blk] = delta;
-      int8_t* out8 = (which == 0 ? args.Q8 : args.K8) + blk * (int64_t)kCap * D;
-      for (int ch = tid; ch < 2 * NS32 * 64; ch += 256) {  // 16-byte chunks
-        const int lane = ch & 63, s = (ch >> 6) % NS32, jq = (ch >> 6) / NS32;
-        const int r = lane & 31, gg = lane >> 5;
-        const int slot = which == 0 ? 32 * jq + r : kappa(jq, r);
-        const float* row = tile + slot * LD + 32 * s + 16 * gg;
-        uint32_t w[4];
-        for (int q = 0; q < 4; ++q) {
-          uint32_t packed = 0;
-          for (int e = 0; e < 4; ++e) {
-            float y = __fmul_rn(row[4 * q + e], inv);
-            float v = fminf(fmaxf(roundf(y), -127.0f), 127.0f);
-            packed |= (static_cast<uint32_t>(static_cast<int>(v)) & 0xFFu) << (8 * e);
-          }
-          w[q] = packed;
-        }
-        *reinterpret_cast<uint4*>(out8 + (int64_t)ch * 16) = make_uint4(w[0], w[1], w[2], w[3]);
-      }
-      // ---- NVFP4 along channels ----
-      _Float16* out4 = (which == 0 ? args.Q4 : args.K4) + blk * (int64_t)kCap * D;
-      for (int ch = tid; ch < 2 * NS16 * 64; ch += 256) {
-        const int lane = ch & 63, s = (ch >> 6) % NS16, jq = (ch >> 6) / NS16;
-        const int r = lane & 31, gg = lane >> 5;
-        const int slot = which == 0 ? 32 * jq + r : kappa(jq, r);
-        const float* grp = tile + slot * LD + 16 * s;
-        float gm = 0.0f;
-        for (int e = 0; e < 16; ++e) gm = fmaxf(gm, fabsf(grp[e]));
-        const float sigma = e4m3_round_mag(__fdiv_rn(gm, sixg));
-        f16x8 o;
-        if (sigma == 0.0f) {
-          for (int e = 0; e < 8; ++e) o[e] = (_Float16)0.0f;
-        } else {
-          const float inv = __fdiv_rn(1.0f, __fmul_rn(gX, sigma));
-          for (int e = 0; e < 8; ++e) o[e] = (_Float16)__fmul_rn(sigma, e2m1_round(__fmul_rn(grp[8 * gg + e], inv)));
-        }
-        *reinterpret_cast<f16x8*>(out4 + (int64_t)ch * 8) = o;
-      }
+  // group u: fragment row rr = 32 jq + r (slot rr for Q, kappa(jq, r) for K),
+  // channels [16 c16, 16 c16 + 16)
+  float x[UPT][16];
+  float amax = 0.0f;
+#pragma unroll
+  for (int k = 0; k < UPT; ++k) {
+    const int u = tid + 256 * k, c16 = u % NG, rr = u / NG;
+    const int slot = which == 0 ? rr : kappa(rr >> 5, rr & 31);
+    if (slot < n) {
+      const T* p = X + (int64_t)slots[slot] * args.sn + 16 * c16;
+#pragma unroll
+      for (int q = 0; q < 16 / EPC; ++q) load_chunk(p + q * EPC, x[k] + q * EPC);
     } else {
-      // ---- E4M3 V, per-channel scale; layout [t][h2][lane][16] ----
-      uint8_t* out8 = args.V8 + blk * (int64_t)kCap * D;
-      for (int ch = tid; ch < NS32 * 2 * 64; ch += 256) {
-        const int lane = ch & 63, h2 = (ch >> 6) & 1, t = ch >> 7;
-        const int c = 32 * t + (lane & 31), s0 = 32 * h2 + 16 * (lane >> 5);
-        const float inv = s_invc[c];
-        uint32_t w[4];
-        for (int q = 0; q < 4; ++q) {
-          uint32_t packed = 0;
-          for (int e = 0; e < 4; ++e) {
-            const uint32_t code = inv == 0.0f ? 0u : e4m3_code(__fmul_rn(tile[(s0 + 4 * q + e) * LD + c], inv));
-            packed |= code << (8 * e);
-          }
-          w[q] = packed;
-        }
-        *reinterpret_cast<uint4*>(out8 + (int64_t)ch * 16) = make_uint4(w[0], w[1], w[2], w[3]);
-      }
-      // ---- NVFP4 V along key slots; layout [t][s:4][lane][8] ----
-      _Float16* out4 = args.V4 + blk * (int64_t)kCap * D;
-      for (int ch = tid; ch < NS32 * 4 * 64; ch += 256) {
-        const int lane = ch & 63, s = (ch >> 6) & 3, t = ch >> 8;
-        const int c = 32 * t + (lane & 31), gg = lane >> 5;
-        const int g0 = 32 * (s >> 1) + 16 * gg;           // first slot of the 16-slot group
-        const int e0 = g0 + 8 * (s & 1);                  // first slot of this chunk
-        float gm = 0.0f;
-        for (int e = 0; e < 16; ++e) gm = fmaxf(gm, fabsf(tile[(g0 + e) * LD + c]));
-        const float sigma = e4m3_round_mag(__fdiv_rn(gm, sixg));
-        f16x8 o;
-        if (sigma == 0.0f) {
-          for (int e = 0; e < 8; ++e) o[e] = (_Float16)0.0f;
-        } else {
-          const float inv = __fdiv_rn(1.0f, __fmul_rn(gX, sigma));
-          for (int e = 0; e < 8; ++e) o[e] = (_Float16)__fmul_rn(sigma, e2m1_round(__fmul_rn(tile[(e0 + e) * LD + c], inv)));
-        }
-        *reinterpret_cast<f16x8*>(out4 + (int64_t)ch * 8) = o;
-      }
-      if (a == 0) {
-        if (tid < D) {
-          args.dV[(int64_t)bh * D + tid] = __fdiv_rn(__uint_as_float(st[4 + tid]), 2.25f);
-        }
-        if (tid < 4) {
-          args.g[(int64_t)bh * 4 + tid] = tid < 3 ? nvfp4_scale_global(st[tid]) : 0.0f;
-        }
-      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) x[k][e] = 0.0f;
     }
-    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(x[k][e]));
+  }
+  amax = wave_max(amax);
+  if ((tid & 63) == 0) s_red[tid >> 6] = amax;
+  __syncthreads();
+  const float bmax = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
+  const float delta = __fadd_rn(__fdiv_rn(bmax, 127.0f), 1e-7f);
+  const float inv8 = __fdiv_rn(1.0f, delta);
+  if (tid == 0) (which == 0 ? args.dQ : args.dK)[blk] = delta;
+  const float gX = nvfp4_scale_global(args.stats[(int64_t)bh * (4 + D) + which]);
+  const float sixg = __fmul_rn(6.0f, gX);
+  int8_t* out8 = (which == 0 ? args.Q8 : args.K8) + blk * (int64_t)kCap * D;
+  _Float16* out4 = (which == 0 ? args.Q4 : args.K4) + blk * (int64_t)kCap * D;
+#pragma unroll
+  for (int k = 0; k < UPT; ++k) {
+    const int u = tid + 256 * k, c16 = u % NG, rr = u / NG;
+    const int jq = rr >> 5, r = rr & 31;
+    // INT8 chunk: [jq][c16/2][lane = r + 32 (c16%2)][16]
+    const int64_t c8 = ((int64_t)(jq * NS32 + (c16 >> 1)) * 64 + r + 32 * (c16 & 1)) * 16;
+    *reinterpret_cast<uint4*>(out8 + c8) = int8_codes16(x[k], inv8);
+    // NVFP4 chunks: [jq][c16][lane = r + 32 g][8] for halves g = 0, 1
+    uint4 lo, hi;
+    nvfp4_group16(x[k], gX, sixg, lo, hi);
+    const int64_t c4 = ((int64_t)(jq * NG + c16) * 64 + r) * 8;
+    *reinterpret_cast<uint4*>(out4 + c4) = lo;
+    *reinterpret_cast<uint4*>(out4 + c4 + 32 * 8) = hi;
   }
 }
 
-hipError_t launch_prep(const PrepArgs& args, hipStream_t stream) {
+// ---- V ------------------------------------------------------------------------
+// Two channels (2p, 2p+1) of slot s from the LDS tile, as floats.
+__device__ inline float2 tile_pair(const uint16_t* tile, int D, int s, int p) {
+  const uint32_t w = reinterpret_cast<const uint32_t*>(tile + s * D)[p];
+  return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+}
+__device__ inline float2 tile_pair(const float* tile, int D, int s, int p) {
+  return reinterpret_cast<const float2*>(tile + s * D)[p];
+}
+
+template <int D, typename T>
+__global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
+  constexpr int EPC = 16 / sizeof(T);
+  constexpr int CPR = D / EPC;
+  constexpr int LPT = kCap * CPR / 256;  // 16-byte loads per thread
+  __shared__ __align__(16) T tile[kCap * D];
+  const int a = blockIdx.x, bh = blockIdx.y;
+  const int b = bh / args.H, h = bh % args.H, R = args.R, tid = threadIdx.x;
+  const Layout L = layout_view(args.layout, R, args.Npad);
+  const int n = L.n_a[a];
+  const int32_t* slots = L.slot2tok + (int64_t)a * kCap;
+  const T* X = static_cast<const T*>(args.V) + (int64_t)b * args.sb + (int64_t)h * args.sh;
+  const uint32_t* st = args.stats + (int64_t)bh * (4 + D);
+  const int64_t blk = (int64_t)bh * R + a;
+
+  uint4 v[LPT];
+#pragma unroll
+  for (int k = 0; k < LPT; ++k) {
+    const int ci = tid + 256 * k, s = ci / CPR, cc = ci % CPR;
+    v[k] = s < n ? *reinterpret_cast<const uint4*>(X + (int64_t)slots[s] * args.sn + cc * EPC) : make_uint4(0u, 0u, 0u, 0u);
+  }
+#pragma unroll
+  for (int k = 0; k < LPT; ++k) {
+    const int ci = tid + 256 * k;
+    reinterpret_cast<uint4*>(tile)[ci] = v[k];
+  }
+  __syncthreads();
+
+  // unit: channel pair p, 16-slot group sg
+  const int p = tid % (D / 2), sg = tid / (D / 2);
+  if (sg < 4) {
+    float x0[16], x1[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float2 f = tile_pair(tile, D, 16 * sg + i, p);
+      x0[i] = f.x;
+      x1[i] = f.y;
+    }
+    const float gV = nvfp4_scale_global(st[2]);
+    const float sixg = __fmul_rn(6.0f, gV);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const float* xc = q == 0 ? x0 : x1;
+      const int c = 2 * p + q;
+      const int lane = (c & 31) + 32 * (sg & 1), t = c >> 5;
+      // E4M3, per-channel scale: chunk [t][h = sg/2][lane][16]
+      const float dlt = __fdiv_rn(__uint_as_float(st[4 + c]), 2.25f);
+      uint4 code = make_uint4(0u, 0u, 0u, 0u);
+      if (dlt != 0.0f) {
+        const float inv = __fdiv_rn(1.0f, dlt);
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          int lo = __builtin_amdgcn_cvt_pk_fp8_f32(__fmul_rn(xc[4 * j], inv), __fmul_rn(xc[4 * j + 1], inv), 0, false);
+          w[j] = static_cast<uint32_t>(__builtin_amdgcn_cvt_pk_fp8_f32(__fmul_rn(xc[4 * j + 2], inv),
+                                                                       __fmul_rn(xc[4 * j + 3], inv), lo, true));
+        }
+        code = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+      *reinterpret_cast<uint4*>(args.V8 + blk * (int64_t)kCap * D + ((int64_t)(2 * t + (sg >> 1)) * 64 + lane) * 16) = code;
+      // NVFP4 along slots: chunks [t][s = 2 (sg/2) + half][lane][8]
+      uint4 lo, hi;
+      nvfp4_group16(xc, gV, sixg, lo, hi);
+      _Float16* o4 = args.V4 + blk * (int64_t)kCap * D + ((int64_t)(4 * t + 2 * (sg >> 1)) * 64 + lane) * 8;
+      *reinterpret_cast<uint4*>(o4) = lo;
+      *reinterpret_cast<uint4*>(o4 + 64 * 8) = hi;
+    }
+  }
+  if (a == 0) {
+    if (tid < D) args.dV[(int64_t)bh * D + tid] = __fdiv_rn(__uint_as_float(st[4 + tid]), 2.25f);
+    if (tid < 4) args.g[(int64_t)bh * 4 + tid] = tid < 3 ? nvfp4_scale_global(st[tid]) : 0.0f;
+  }
+}
+
+template <int D, typename T>
+void launch_prep_t(const PrepArgs& args, hipStream_t stream) {
   const int BH = args.B * args.H;
   hipLaunchKernelGGL(zero_vstats_kernel, dim3(BH), dim3(64), 0, stream, args.stats, args.d);
+  hipLaunchKernelGGL((prep_vstats_kernel<D, T>), dim3((args.N + kVstatRows - 1) / kVstatRows, BH), dim3(256), 0,
+                     stream, args);
+  hipLaunchKernelGGL((prep_qk_kernel<D, T>), dim3(args.R, BH, 2), dim3(256), 0, stream, args);
+  hipLaunchKernelGGL((prep_v_kernel<D, T>), dim3(args.R, BH), dim3(256), 0, stream, args);
+}
+
+hipError_t launch_prep(const PrepArgs& args, hipStream_t stream) {
   if (args.d == 128) {
-    hipLaunchKernelGGL(prep_vstats_kernel<128>, dim3(args.R, BH), dim3(256), 0, stream, args);
-    hipLaunchKernelGGL(prep_encode_kernel<128>, dim3(args.R, BH), dim3(256), 0, stream, args);
+    if (args.dtype == DA2_BF16)
+      launch_prep_t<128, uint16_t>(args, stream);
+    else
+      launch_prep_t<128, float>(args, stream);
   } else {
-    hipLaunchKernelGGL(prep_vstats_kernel<64>, dim3(args.R, BH), dim3(256), 0, stream, args);
-    hipLaunchKernelGGL(prep_encode_kernel<64>, dim3(args.R, BH), dim3(256), 0, stream, args);
+    if (args.dtype == DA2_BF16)
+      launch_prep_t<64, uint16_t>(args, stream);
+    else
+      launch_prep_t<64, float>(args, stream);
   }
   return hipGetLastError();
 }

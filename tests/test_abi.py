@@ -120,6 +120,28 @@ def test_compute_calls_validate_before_gpu():
     assert L.da2_mixed_attn(FAKE, FAKE, FAKE, p, _desc(dtype=9), FAKE, None) == E
 
 
+def test_inputs_must_allow_16_byte_loads():
+    """Q, K, V are read in 16-byte vectors: misaligned bases or strides that
+    are not a multiple of 16 bytes are rejected before any GPU work."""
+    L = _lib.lib()
+    p = _p(configs.MID)
+    s = api.da2_sizes(p)
+    E = _lib.DA2_ERR_INVALID_ARG
+    odd = ctypes.c_void_p(0x1000 + 2)
+    ws = s["ws_draft_bytes"]
+    assert L.da2_draft_map(odd, FAKE, _desc(), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
+    assert L.da2_draft_map(FAKE, odd, _desc(), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, odd, _desc(), FAKE, p, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_draft_map(FAKE, FAKE, _desc(sn=132), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(sn=130), FAKE, p, FAKE, FAKE, None, 0, None) == E
+    f32 = _lib.Tensor(12 * 32760 * 128 + 2, 32760 * 128, 128, _lib.DA2_FP32, 0)
+    assert L.da2_draft_map(FAKE, FAKE, f32, FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
+    # fp32 rows need only 4-element alignment: the stride check passes and the
+    # (deliberately short) workspace is what gets reported
+    ok32 = _lib.Tensor(12 * 32760 * 132, 32760 * 132, 132, _lib.DA2_FP32, 0)
+    assert L.da2_draft_map(FAKE, FAKE, ok32, FAKE, p, 0.2, FAKE, FAKE, FAKE, ws - 1, None) == _lib.DA2_ERR_WORKSPACE
+
+
 @pytest.mark.skipif(os.path.exists("/dev/kfd"), reason="checks the no-GPU path")
 def test_no_device_is_reported_not_crashed():
     L = _lib.lib()

@@ -73,7 +73,8 @@ def test_hardware_fp8_conversion_is_rne_in_range(probe):
 
 def test_hardware_fp4_conversion(probe):
     """v_cvt_scalef32_pk_fp4_f32 then v_cvt_scalef32_pk_f16_fp4, unit scales:
-    round to nearest even with saturation, like the E2M1 cast definition."""
+    round to nearest even with saturation and signed zeros, like the E2M1 cast
+    definition."""
     x, o = probe
     want = F.e2m1(x)
     bad = np.nonzero(o["e2m1_hw"] != want)[0]
@@ -83,6 +84,9 @@ def test_hardware_fp4_conversion(probe):
     s2_mul = np.mean(o["e2m1_hw_s2"] == F.e2m1(x * 2))
     b3_full = np.mean(o["e2m1_hw_back3"] == F.e2m1(x) * 3)
     b3_exp = np.mean(o["e2m1_hw_back3"] == F.e2m1(x) * 2)
+    # the operand encoder relies on E2M1 zeros keeping the sign of their input
+    zero = want == 0
+    assert np.array_equal(np.signbit(o["e2m1_hw"][zero]), np.signbit(want[zero]))
     print(f"encode scale 2: matches x/2 {s2_div:.4f}, x*2 {s2_mul:.4f}; "
           f"decode scale 3: full {b3_full:.4f}, exponent only {b3_exp:.4f}")
     assert bad.size == 0
