@@ -83,26 +83,40 @@ __device__ inline float max16(const f32x16& v) {
 
 constexpr float kLog2_2688 = 11.392317422778760f;  // log2(6 * 448)
 
-// NVFP4 weights of one 16-slot group held by this lane (slots of S[0..15]):
-// sigma_P = E4M3(448 max Pt), w = sigma_P * E2M1(Pt * 2688 / sigma_P) as fp16
-// pairs for the P^T operand; returns the fp32 sum of Pt. The scaled weights
-// y = Pt * 2688 / sigma_P come from one exp2 each (the factor is folded into
-// the exponent); a zero sigma_P uses factor 1, and those y (all below 2^-18)
-// round to E2M1 zero as the format requires.
-__device__ inline float nvfp4_weights(const f32x16& S, float c, float mn, float gmax, f16x8& lo, f16x8& hi) {
+// NVFP4 weights of one 16-slot group held by this lane (slots of S[0..15]),
+// computed in stages so that they can be interleaved with matrix work:
+//   setup: sigma_P = E4M3(448 max Pt) from the group's maximum logit;
+//   exps:  y = Pt * 2688 / sigma_P from one exp2 each (the factor is folded
+//          into the exponent) and their fp32 sum;
+//   pack:  w = sigma_P * E2M1(y) as fp16 pairs for the P^T operand (exact:
+//          at most 6 significant bits).
+// A zero sigma_P uses factor 1, and those y (all below 2^-18) round to E2M1
+// zero as the format requires. weight_sum() is the fp32 sum of Pt.
+struct Fp4Group {
+  float off, scale, sum;
+  f16x2 s2;
+  float y[16];
+};
+__device__ inline void fp4_setup(Fp4Group& G, float gmax, float c, float mn) {
   const float pmax = exp2_fast(__builtin_fmaf(gmax, c, -mn));
   const float sigma = e4m3_round_mag(fminf(448.0f * pmax, 448.0f));
   const bool nz = sigma > 0.0f;
-  const float off = (nz ? kLog2_2688 - __builtin_amdgcn_logf(sigma) : 0.0f) - mn;
+  G.off = (nz ? kLog2_2688 - __builtin_amdgcn_logf(sigma) : 0.0f) - mn;
+  G.scale = nz ? sigma * (1.0f / 2688.0f) : 1.0f;
   const _Float16 sh = (_Float16)sigma;
-  const f16x2 s2 = {sh, sh};
-  float y[16];
-  float sum = 0.0f;
+  G.s2 = f16x2{sh, sh};
+  G.sum = 0.0f;
+}
+template <int I0, int I1>
+__device__ inline void fp4_exps(Fp4Group& G, const f32x16& S, float c) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    y[i] = exp2_fast(__builtin_fmaf(S[i], c, off));
-    sum += y[i];
+  for (int i = I0; i < I1; ++i) {
+    G.y[i] = exp2_fast(__builtin_fmaf(S[i], c, G.off));
+    G.sum += G.y[i];
   }
+}
+__device__ inline void fp4_pack(const Fp4Group& G, f16x8& lo, f16x8& hi) {
+  const float* y = G.y;
   // E2M1 codes, two per byte (byte selector must be a literal)
   uint32_t f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
   f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, y[2], y[3], 1.0f, 1);
@@ -112,7 +126,7 @@ __device__ inline float nvfp4_weights(const f32x16& S, float c, float mn, float 
   f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[10], y[11], 1.0f, 1);
   f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[12], y[13], 1.0f, 2);
   f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[14], y[15], 1.0f, 3);
-  // back to fp16 and times sigma_P (exact: at most 6 significant bits)
+  const f16x2 s2 = G.s2;
   const f16x2 a0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 0) * s2;
   const f16x2 a1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 1) * s2;
   const f16x2 a2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 2) * s2;
@@ -123,16 +137,40 @@ __device__ inline float nvfp4_weights(const f32x16& S, float c, float mn, float 
   const f16x2 b3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f1, 1.0f, 3) * s2;
   lo = f16x8{a0[0], a0[1], a1[0], a1[1], a2[0], a2[1], a3[0], a3[1]};
   hi = f16x8{b0[0], b0[1], b1[0], b1[1], b2[0], b2[1], b3[0], b3[1]};
-  return sum * (nz ? sigma * (1.0f / 2688.0f) : 1.0f);
+}
+__device__ inline float weight_sum(const Fp4Group& G) { return G.sum * G.scale; }
+
+// INT8-path weights of 8 logits S[I0..I0+8) of this lane: amplified weights
+// 2^((s - m) log2 e + 8.807) in E4M3 (two dwords of the fp8 P^T operand);
+// returns their fp32 sum.
+template <int I0>
+__device__ inline float fp8_weights8(const f32x16& S, float cb, float off, int& w0, int& w1) {
+  float p[8];
+  float sum = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    p[e] = exp2_fast(__builtin_fmaf(S[I0 + e], cb, off));
+    sum += p[e];
+  }
+  w0 = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], 0, false), true);
+  w1 = __builtin_amdgcn_cvt_pk_fp8_f32(p[6], p[7], __builtin_amdgcn_cvt_pk_fp8_f32(p[4], p[5], 0, false), true);
+  return sum;
 }
 
+// Scheduling fence: no instruction moves across it, so the stages between two
+// fences keep the interleaving of matrix and vector work written in the source.
+__device__ inline void fence() { __builtin_amdgcn_sched_barrier(0); }
+
 // Padded key slots (slot >= nb) of a partial block get -inf logits.
+// Register i of logit tile j holds slot 32j + 16g + i.
 __device__ inline void mask_tail(f32x16 (&S)[2], int nb, int g) {
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
+  for (int j = 0; j < 2; ++j) {
+    const int valid = nb - 32 * j - 16 * g;  // valid registers of this lane
 #pragma unroll
     for (int i = 0; i < 16; ++i)
-      if (32 * j + 16 * g + i >= nb) S[j][i] = -INFINITY;
+      if (i >= valid) S[j][i] = -INFINITY;
+  }
 }
 
 // Key-list window: lane i holds entry first+i of the row's list of key blocks
@@ -179,109 +217,97 @@ __device__ inline void wg_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Softmax of this wave's 32-query tile on the NVFP4 path: running max, NVFP4
-// weights, denominator; the numerator's rescale factor comes back in alpha.
-__device__ inline void softmax_fp4(f32x16 (&S)[2], int nb, int g, float c4, float& m, float& l, float& alpha,
-                                   f16x8 (&Pf)[4]) {
-  if (nb < kCap) mask_tail(S, nb, g);
-  const float gm0 = max16(S[0]), gm1 = max16(S[1]);
-  const float mn = new_max(fmaxf(gm0, gm1), c4, m, l, alpha);
-  const float s0 = nvfp4_weights(S[0], c4, mn, gm0, Pf[0], Pf[1]);
-  const float s1 = nvfp4_weights(S[1], c4, mn, gm1, Pf[2], Pf[3]);
-  l += s0 + s1;
-}
-
-// Softmax of this wave's 32-query tile on the INT8 path: amplified weights
-// 2^((s - m) log2 e + 8.807) in E4M3 for the fp8 P^T operand.
-__device__ inline void softmax_fp8(const i32x16 (&Si)[2], int nb, int g, float cb, float& m, float& l, float& alpha,
-                                   i32x8& Pf) {
-  f32x16 sf[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) sf[j][i] = (float)Si[j][i];
-  if (nb < kCap) mask_tail(sf, nb, g);
-  const float mn = new_max(fmaxf(max16(sf[0]), max16(sf[1])), cb, m, l, alpha);
-  const float off = kExpOffset - mn;
-  float lsum = 0.0f;
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      float p[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        p[e] = exp2_fast(__builtin_fmaf(sf[j][4 * w + e], cb, off));
-        lsum += p[e];
-      }
-      const int v = __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], 0, false);
-      Pf[4 * j + w] = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], v, true);
-    }
-  l += lsum;
-}
-
-// One precision phase of the block loop. The workgroup's two waves own the
-// query tiles qt = 0, 1 of the block; the key and value tiles of each key
-// block are copied into LDS once (each wave issues half of the fragments) and
-// read by both waves. Per block i:
-//   wait K(i) -> barrier -> S = K Q^T -> barrier -> DMA K(i+1)
-//   softmax (overlaps the K(i+1) and V(i) copies)
-//   wait V(i) -> barrier -> U += V^T P^T -> barrier -> DMA V(i+1)
-// Frag: fragment type; NFK/NFV: fragments per K/V tile.
 // Orders a wait after the computation of v (an empty use of the register).
 template <typename T>
 __device__ inline void after(const T& v) {
   asm volatile("" ::"v"(v));
 }
 
-template <int NFK, int NFV, typename Frag, typename QK, typename SM, typename PV>
+// One precision phase of the block loop, software-pipelined by one block: the
+// logits of block i+1 are computed while the softmax of block i runs, so the
+// matrix cores and the vector ALUs work side by side inside each wave. The
+// workgroup's two waves own the query tiles qt = 0, 1 of the query block; the
+// key and value tiles of each key block are copied into LDS once (each wave
+// issues half of the fragments) and read by both waves. Iteration i:
+//   wait K(i+1) -> barrier -> S' = K(i+1) Q^T interleaved with the softmax of S
+//   -> barrier -> DMA K(i+2) -> wait V(i) -> barrier -> U += V(i)^T P^T
+//   -> barrier -> DMA V(i+1)
+// Frag: fragment type; NFK: fragments per K (and V) tile; SA: logit tile type.
+// first(S): logits of the first block. step<MASK>(S, S', nb, dk): the
+// interleaved region (MASK: block i is partial). pv(): the value product.
+template <int NFK, typename Frag, typename SA, typename FIRST, typename STEP, typename PV>
 __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_a, const float* dKh,
                                   const Frag* Kh, const Frag* Vh, Frag* sK, Frag* sV, int wave, int lane,
-                                  QK qk, SM softmax, PV pv) {
-  constexpr int TILE = NFK * 64;  // fragments per block, in Frag units (K and V have the same size)
-  static_assert(NFK == NFV, "K and V tiles hold the same number of fragments");
-  constexpr int HALF = NFK / 2;
+                                  FIRST first_qk, STEP region, PV pv) {
+  constexpr int TILE = NFK * 64;  // fragments per tile
+  constexpr int HALF = NFK / 2;   // fragments each wave copies
   auto dma_tile = [&](const Frag* src, Frag* dst) {
 #pragma unroll
     for (int f = wave * HALF; f < (wave + 1) * HALF; ++f) dma_fragment(src + f * 64 + lane, dst + f * 64);
   };
   KeyWin win = key_window(list, 0, n, n_a, dKh, lane);
-  dma_tile(Kh + (int64_t)lane_value(win.kb, 0) * TILE, sK);
-  dma_tile(Vh + (int64_t)lane_value(win.kb, 0) * TILE, sV);
-  for (int it = 0; it < n; ++it) {
-    const int sl = it & 63;
+  // key block of list entry e, first being the current window's first entry
+  auto block_at = [&](int e, int first) -> int {
+    return e - first < 64 ? lane_value(win.kb, e - first) : (int)list[e];
+  };
+  // prologue: logits of block 0, then K(1) and V(0) in flight
+  const int kb0 = lane_value(win.kb, 0);
+  dma_tile(Kh + (int64_t)kb0 * TILE, sK);
+  wait_vmem_keep<0>();
+  wg_barrier();
+  SA Sa, Sb;
+  first_qk(Sa);
+  wait_lds();
+  wg_barrier();
+  if (n > 1) dma_tile(Kh + (int64_t)block_at(1, 0) * TILE, sK);
+  dma_tile(Vh + (int64_t)kb0 * TILE, sV);
+
+  auto step = [&](int it, SA& Sc, SA& Sn) {
+    const int first = it & ~63;
+    const int sl = it - first;
     if (sl == 0 && it > 0) win = key_window(list, it, n, n_a, dKh, lane);
-    const int kb = lane_value(win.kb, sl);
     const int nb = lane_value(win.nb, sl);
     const float dk = lane_value(win.dk, sl);
-    const bool more = it + 1 < n;
-    const int kb_next = !more ? 0 : (sl < 63 ? lane_value(win.kb, sl + 1) : (int)list[it + 1]);
-    wait_vmem_keep<HALF>();  // K(i) copied (V(i), issued later, may still be in flight)
+    const bool more1 = it + 1 < n, more2 = it + 2 < n;
+    const int kb1 = more1 ? block_at(it + 1, first) : 0;
+    const int kb2 = more2 ? block_at(it + 2, first) : 0;
+    // K(i+1) copied (V(i), issued later, may still be in flight). On the last
+    // block the logits of the region are computed from the unchanged tile and
+    // not used.
+    wait_vmem_keep<HALF>();
     wg_barrier();
-    qk(nb, dk);
+    if (nb < kCap)
+      region.template operator()<true>(Sc, Sn, nb, dk);
+    else
+      region.template operator()<false>(Sc, Sn, nb, dk);
     wait_lds();
     wg_barrier();  // both waves are done with sK
-    if (more) dma_tile(Kh + (int64_t)kb_next * TILE, sK);
-    softmax(nb, dk);  // returns after its results exist, so the wait below cannot move above it
-    if (more)
-      wait_vmem_keep<HALF>();  // V(i) copied, K(i+1) may still be in flight
-    else
+    if (more2) {
+      dma_tile(Kh + (int64_t)kb2 * TILE, sK);
+      wait_vmem_keep<HALF>();  // V(i) copied, K(i+2) may still be in flight
+    } else {
       wait_vmem_keep<0>();
+    }
     wg_barrier();
     pv();
     wait_lds();
     wg_barrier();  // both waves are done with sV
-    if (more) dma_tile(Vh + (int64_t)kb_next * TILE, sV);
-    (void)kb;
+    if (more1) dma_tile(Vh + (int64_t)kb1 * TILE, sV);
+  };
+  for (int it = 0; it < n; it += 2) {
+    step(it, Sa, Sb);
+    if (it + 1 < n) step(it + 1, Sb, Sa);
   }
 }
 
 template <int D>
-__global__ __launch_bounds__(128) void mixed_attn_kernel(AttnArgs args) {
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void mixed_attn_kernel(AttnArgs args) {
   constexpr int NS16 = D / 16, NS32 = D / 32, NT = D / 32;
   __shared__ f16x8 sK[2 * NS16 * 64];  // key tile of the current block (16 KB at d=128)
   __shared__ f16x8 sV[NT * 4 * 64];    // value tile of the current block
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, r = lane & 31, g = lane >> 5;
+  // wave index as a uniform (scalar) value: LDS fragment addresses stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, r = lane & 31, g = lane >> 5;
   const int qt = wave;  // this wave's 32-query tile
   const int R = args.R;
   // XCD-aware mapping: workgroup b runs on XCD b mod 8 and takes the next row
@@ -312,10 +338,10 @@ __global__ __launch_bounds__(128) void mixed_attn_kernel(AttnArgs args) {
     const f16x8* Qa = reinterpret_cast<const f16x8*>(args.Q4) + (blk0 + a) * (kCap * D / 8);
 #pragma unroll
     for (int s = 0; s < NS16; ++s) Qf[s] = Qa[(qt * NS16 + s) * 64 + lane];
-    f32x16 S[2];
     f16x8 P[4];
     float alpha = 1.0f;
-    auto qk = [&](int, float) {
+    typedef f32x16 SA[2];
+    auto qk = [&](SA& S) {
       S[0] = S[1] = f32x16{};
 #pragma unroll
       for (int s = 0; s < NS16; ++s)
@@ -323,21 +349,78 @@ __global__ __launch_bounds__(128) void mixed_attn_kernel(AttnArgs args) {
         for (int j = 0; j < 2; ++j)
           S[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sK[(j * NS16 + s) * 64 + lane], Qf[s], S[j], 0, 0, 0);
     };
-    auto sm = [&](int nb, float) {
-      softmax_fp4(S, nb, g, c4, m, l, alpha, P);
+    // Interleaved region: logits of the next block (NS16 stages of two
+    // MFMAs, operands read one stage ahead) with the softmax of the current
+    // one split into 8 pieces over the stages.
+    auto region = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float) {
+      if constexpr (MASK) mask_tail(Sc, nb, g);
+      float gm0 = 0.0f, gm1 = 0.0f, mn = 0.0f;
+      Fp4Group G0, G1;
+      f16x8 k0 = sK[lane], k1 = sK[NS16 * 64 + lane];
+      constexpr int PPS = 8 / NS16;  // softmax pieces per stage
+#pragma unroll
+      for (int s = 0; s < NS16; ++s) {
+        f16x8 n0 = k0, n1 = k1;
+        if (s + 1 < NS16) {
+          n0 = sK[(s + 1) * 64 + lane];
+          n1 = sK[(NS16 + s + 1) * 64 + lane];
+        }
+        Sn[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(k0, Qf[s], s == 0 ? f32x16{} : Sn[0], 0, 0, 0);
+        Sn[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(k1, Qf[s], s == 0 ? f32x16{} : Sn[1], 0, 0, 0);
+#pragma unroll
+        for (int q = 0; q < PPS; ++q) {
+          const int piece = s * PPS + q;
+          if (piece == 0) {
+            gm0 = max16(Sc[0]);
+          } else if (piece == 1) {
+            gm1 = max16(Sc[1]);
+            mn = new_max(fmaxf(gm0, gm1), c4, m, l, alpha);
+          } else if (piece == 2) {
+            fp4_setup(G0, gm0, c4, mn);
+            fp4_exps<0, 4>(G0, Sc[0], c4);
+          } else if (piece == 3) {
+            fp4_exps<4, 10>(G0, Sc[0], c4);
+          } else if (piece == 4) {
+            fp4_exps<10, 16>(G0, Sc[0], c4);
+          } else if (piece == 5) {
+            fp4_pack(G0, P[0], P[1]);
+            fp4_setup(G1, gm1, c4, mn);
+          } else if (piece == 6) {
+            fp4_exps<0, 8>(G1, Sc[1], c4);
+          } else {
+            fp4_exps<8, 16>(G1, Sc[1], c4);
+          }
+        }
+        fence();
+        k0 = n0;
+        k1 = n1;
+      }
+      fp4_pack(G1, P[2], P[3]);
+      l += weight_sum(G0) + weight_sum(G1);
       after(P[0]), after(P[1]), after(P[2]), after(P[3]), after(l);
     };
+    // U += V^T P^T; value fragments are read two MFMAs ahead.
     auto pv = [&]() {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+      constexpr int NM = 4 * NT;
+      auto vfrag = [&](int k) { return sV[((k % NT) * 4 + k / NT) * 64 + lane]; };
+      f16x8 v0 = vfrag(0), v1 = vfrag(1);
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-          U[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sV[(t * 4 + s) * 64 + lane], P[s], U[t], 0, 0, 0);
+      for (int k = 0; k < NM; ++k) {
+        const f16x8 cur = (k & 1) ? v1 : v0;
+        if (k + 2 < NM) {
+          if (k & 1)
+            v1 = vfrag(k + 2);
+          else
+            v0 = vfrag(k + 2);
+        }
+        U[k % NT] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur, P[k / NT], U[k % NT], 0, 0, 0);
+        fence();
+      }
     };
-    phase_loop<2 * NS16, NT * 4>(keys, n4, L.n_a, dKh, reinterpret_cast<const f16x8*>(args.K4) + blk0 * (kCap * D / 8),
+    phase_loop<2 * NS16, f16x8, SA>(keys, n4, L.n_a, dKh, reinterpret_cast<const f16x8*>(args.K4) + blk0 * (kCap * D / 8),
                                  reinterpret_cast<const f16x8*>(args.V4) + blk0 * (kCap * D / 8), sK, sV, wave, lane,
-                                 qk, sm, pv);
+                                 qk, region, pv);
   }
 
   // per-lane channel of accumulator register i of channel tile t
@@ -365,10 +448,10 @@ __global__ __launch_bounds__(128) void mixed_attn_kernel(AttnArgs args) {
     const float c8a = args.dQ[blk0 + a] * kLog2e * rsqd;
     i32x4* sK8 = reinterpret_cast<i32x4*>(sK);
     i32x4* sV8 = reinterpret_cast<i32x4*>(sV);
-    i32x16 S[2];
     i32x8 P;
     float alpha = 1.0f;
-    auto qk = [&](int, float) {
+    typedef i32x16 SA[2];
+    auto qk = [&](SA& S) {
       S[0] = S[1] = i32x16{};
 #pragma unroll
       for (int s = 0; s < NS32; ++s)
@@ -376,25 +459,72 @@ __global__ __launch_bounds__(128) void mixed_attn_kernel(AttnArgs args) {
         for (int j = 0; j < 2; ++j)
           S[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(sK8[(j * NS32 + s) * 64 + lane], Qf[s], S[j], 0, 0, 0);
     };
-    auto sm = [&](int nb, float dk) {
-      softmax_fp8(S, nb, g, c8a * dk, m, l, alpha, P);
+    // Interleaved region: logits of the next block (NS32 stages of two int8
+    // MFMAs) with the softmax of the current one in 4 pieces.
+    auto region = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float dk) {
+      const float cb = c8a * dk;
+      f32x16 sf[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sf[j][i] = (float)Sc[j][i];
+      if constexpr (MASK) mask_tail(sf, nb, g);
+      float off = 0.0f, s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+      int w[8];
+      i32x4 k0 = sK8[lane], k1 = sK8[NS32 * 64 + lane];
+      constexpr int PPS = 4 / NS32;
+#pragma unroll
+      for (int s = 0; s < NS32; ++s) {
+        i32x4 n0 = k0, n1 = k1;
+        if (s + 1 < NS32) {
+          n0 = sK8[(s + 1) * 64 + lane];
+          n1 = sK8[(NS32 + s + 1) * 64 + lane];
+        }
+        Sn[0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(k0, Qf[s], s == 0 ? i32x16{} : Sn[0], 0, 0, 0);
+        Sn[1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(k1, Qf[s], s == 0 ? i32x16{} : Sn[1], 0, 0, 0);
+#pragma unroll
+        for (int q = 0; q < PPS; ++q) {
+          const int piece = s * PPS + q;
+          if (piece == 0) {
+            off = kExpOffset - new_max(fmaxf(max16(sf[0]), max16(sf[1])), cb, m, l, alpha);
+          } else if (piece == 1) {
+            s0 = fp8_weights8<0>(sf[0], cb, off, w[0], w[1]);
+            s1 = fp8_weights8<8>(sf[0], cb, off, w[2], w[3]);
+          } else if (piece == 2) {
+            s2 = fp8_weights8<0>(sf[1], cb, off, w[4], w[5]);
+            s3 = fp8_weights8<8>(sf[1], cb, off, w[6], w[7]);
+          }
+        }
+        fence();
+        k0 = n0;
+        k1 = n1;
+      }
+      P = i32x8{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]};
+      l += (s0 + s1) + (s2 + s3);
       after(P), after(l);
     };
+    // U += V^T P^T (fp8 x fp8, unit scales); value fragments read one MFMA ahead.
     auto pv = [&]() {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+      auto vfrag = [&](int t) {
+        const i32x4 v0 = sV8[(t * 2 + 0) * 64 + lane], v1 = sV8[(t * 2 + 1) * 64 + lane];
+        return i32x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+      };
+      i32x8 vf = vfrag(0);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const i32x4 v0 = sV8[(t * 2 + 0) * 64 + lane], v1 = sV8[(t * 2 + 1) * 64 + lane];
-        const i32x8 vf = i32x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-        U[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vf, P, U[t], 0, 0, 0, 127, 0, 127);
+        const i32x8 cur = vf;
+        if (t + 1 < NT) vf = vfrag(t + 1);
+        U[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur, P, U[t], 0, 0, 0, 127, 0, 127);
+        fence();
       }
     };
     wait_lds();
     wg_barrier();  // the NVFP4 phase is done with sK / sV
-    phase_loop<2 * NS32, NT * 2>(keys + n4, n8, L.n_a, dKh,
+    phase_loop<2 * NS32, i32x4, SA>(keys + n4, n8, L.n_a, dKh,
                                  reinterpret_cast<const i32x4*>(args.K8) + blk0 * (kCap * D / 16),
                                  reinterpret_cast<const i32x4*>(args.V8) + blk0 * (kCap * D / 16), sK8, sV8, wave,
-                                 lane, qk, sm, pv);
+                                 lane, qk, region, pv);
     // Exit: U_c <- eta delta_c U_c, l <- eta l
 #pragma unroll
     for (int t = 0; t < NT; ++t)
