@@ -85,7 +85,8 @@ const char* da2_status_string(int32_t status);
 
 /* Host only. Fills *out for problem p; ranking scope affects ws_rank_bytes.
  * Errors: INVALID_ARG for non-positive dims, d not in {64,128}, or sizes that
- * overflow the index types (R > 65535 blocks, B*H*R > 2^31-1). */
+ * overflow the index types or launch grids (R > 65535 blocks, B*H > 32767,
+ * B*H*R > 2^31-1). */
 int32_t da2_sizes(const da2_problem* p, int32_t scope, da2_sizes_t* out);
 
 /* Host only: region layout (fused-preparation section: each region packed

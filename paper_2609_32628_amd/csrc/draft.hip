@@ -3,9 +3,9 @@
 //   draft_pool     one workgroup per (block, head, Q or K): mean (float64 sum /
 //                  n_a) and channel max over the valid tokens, plus the per-head
 //                  max|Q|, max|K| used by the NVFP4 tensor scales.
-//   draft_logits   64x64 tiles of Qbar Kbar^T / sqrt d and Qmax Kmax^T / sqrt d in
-//                  float64, both operands staged through LDS in 16-channel slices.
-//   draft_softmax  one workgroup per row: the two row softmaxes (max subtracted)
+//   draft_logits   64x64 tiles of Qbar Kbar^T / sqrt d or Qmax Kmax^T / sqrt d on
+//                  the float64 matrix cores (16x16x4 MFMA).
+//   draft_softmax  one wave per row: the two row softmaxes (max subtracted)
 //                  mixed with weight lambda, rounded once to float32.
 #include "common.hpp"
 #include "launch.hpp"
@@ -94,89 +94,92 @@ __global__ __launch_bounds__(256) void draft_pool_kernel(DraftArgs args) {
   }
 }
 
-// 64x64 logit tile of both branches; 256 threads, 4x4 outputs per thread per branch.
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+// One 64x64 logit tile of one branch (blockIdx.z = 2*head + branch) on the
+// float64 matrix cores: each wave owns a 32x32 quarter as 2x2 MFMA tiles of
+// 16x16x4. The reduction over channels may visit them in any order as long as
+// both operands agree: lane group q = lane/16 of k-step 2t+h reads channel
+// 8t + 2q + h, so one 16-byte load per operand tile feeds two k-steps. Rows
+// and columns beyond R read row R-1 and are not stored.
 __global__ __launch_bounds__(256) void draft_logits_kernel(DraftArgs args) {
-  constexpr int KC = 16;
-  __shared__ double sA[2][64][KC + 1];
-  __shared__ double sB[2][64][KC + 1];
-  const int R = args.R, d = args.d, bh = blockIdx.z;
-  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
-  const double* Qs[2] = {args.Qbar + (int64_t)bh * R * d, args.Qmax + (int64_t)bh * R * d};
-  const double* Ks[2] = {args.Kbar + (int64_t)bh * R * d, args.Kmax + (int64_t)bh * R * d};
-  double acc[2][4][4] = {};
-  for (int k0 = 0; k0 < d; k0 += KC) {
-    for (int e = threadIdx.x; e < 64 * KC; e += 256) {
-      int row = e / KC, kk = e % KC;
-      for (int br = 0; br < 2; ++br) {
-        sA[br][row][kk] = (r0 + row < R) ? Qs[br][(int64_t)(r0 + row) * d + k0 + kk] : 0.0;
-        sB[br][row][kk] = (c0 + row < R) ? Ks[br][(int64_t)(c0 + row) * d + k0 + kk] : 0.0;
-      }
-    }
-    __syncthreads();
-#pragma unroll 4
-    for (int kk = 0; kk < KC; ++kk) {
+  const int R = args.R, d = args.d, bh = blockIdx.z >> 1, br = blockIdx.z & 1;
+  const double* Qs = (br == 0 ? args.Qbar : args.Qmax) + (int64_t)bh * R * d;
+  const double* Ks = (br == 0 ? args.Kbar : args.Kmax) + (int64_t)bh * R * d;
+  double* out = (br == 0 ? args.S1 : args.S2) + (int64_t)bh * R * R;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, li = lane & 15, q = lane >> 4;
+  const int r0 = blockIdx.y * 64 + (wave >> 1) * 32, c0 = blockIdx.x * 64 + (wave & 1) * 32;
+  const double* pa[2];
+  const double* pb[2];
 #pragma unroll
-      for (int br = 0; br < 2; ++br) {
-        double av[4], bv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) av[i] = sA[br][ty + 16 * i][kk];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) bv[j] = sB[br][tx + 16 * j][kk];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[br][i][j] = __builtin_fma(av[i], bv[j], acc[br][i][j]);
-      }
-    }
-    __syncthreads();
+  for (int i = 0; i < 2; ++i) {
+    pa[i] = Qs + (int64_t)min(r0 + 16 * i + li, R - 1) * d + 2 * q;
+    pb[i] = Ks + (int64_t)min(c0 + 16 * i + li, R - 1) * d + 2 * q;
   }
+  f64x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+  for (int t = 0; t < d; t += 8) {
+    double2 a[2], b[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      a[i] = *reinterpret_cast<const double2*>(pa[i] + t);
+      b[i] = *reinterpret_cast<const double2*>(pb[i] + t);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i].x, b[j].x, acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i].y, b[j].y, acc[i][j], 0, 0, 0);
+      }
+  }
+  // accumulator element e of lane l: row l/16 + 4e, column l%16
   const double sqd = sqrt((double)d);
-  double* outs[2] = {args.S1 + (int64_t)bh * R * R, args.S2 + (int64_t)bh * R * R};
-  for (int br = 0; br < 2; ++br)
-    for (int i = 0; i < 4; ++i)
-      for (int j = 0; j < 4; ++j) {
-        int r = r0 + ty + 16 * i, cc = c0 + tx + 16 * j;
-        if (r < R && cc < R) outs[br][(int64_t)r * R + cc] = acc[br][i][j] / sqd;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = r0 + 16 * i + q + 4 * e, col = c0 + 16 * j + li;
+        if (row < R && col < R) out[(int64_t)row * R + col] = acc[i][j][e] / sqd;
       }
 }
 
-__device__ inline double block_reduce(double v, bool is_max, double* sh) {
-  for (int o = 32; o > 0; o >>= 1) {
-    double w = __shfl_xor(v, o, 64);
-    v = is_max ? fmax(v, w) : v + w;
-  }
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
-  __syncthreads();
-  double r = sh[0];
-  for (int q = 1; q < (int)(blockDim.x >> 6); ++q) r = is_max ? fmax(r, sh[q]) : r + sh[q];
-  return r;
+__device__ inline double wave_max_f64(double v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
+  return v;
 }
 
+// One wave per row of A (four rows per workgroup): the two row softmaxes (max
+// subtracted) mixed with weight lambda, rounded once to float32.
 __global__ __launch_bounds__(256) void draft_softmax_kernel(DraftArgs args) {
-  __shared__ double sh[4];
-  const int R = args.R, a = blockIdx.x, bh = blockIdx.y;
-  const double* s1 = args.S1 + ((int64_t)bh * R + a) * R;
-  const double* s2 = args.S2 + ((int64_t)bh * R + a) * R;
+  const int R = args.R, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= (int64_t)args.B * args.H * R) return;
+  const double* s1 = args.S1 + row * R;
+  const double* s2 = args.S2 + row * R;
   double m1 = -INFINITY, m2 = -INFINITY;
-  for (int i = threadIdx.x; i < R; i += 256) {
+  for (int i = lane; i < R; i += 64) {
     m1 = fmax(m1, s1[i]);
     m2 = fmax(m2, s2[i]);
   }
-  m1 = block_reduce(m1, true, sh);
-  m2 = block_reduce(m2, true, sh);
+  m1 = wave_max_f64(m1);
+  m2 = wave_max_f64(m2);
   double z1 = 0.0, z2 = 0.0;
-  for (int i = threadIdx.x; i < R; i += 256) {
+  for (int i = lane; i < R; i += 64) {
     z1 += exp(s1[i] - m1);
     z2 += exp(s2[i] - m2);
   }
-  z1 = block_reduce(z1, false, sh);
-  z2 = block_reduce(z2, false, sh);
+  z1 = wave_sum_f64(z1);
+  z2 = wave_sum_f64(z2);
   const double lam = args.lambda;
-  float* out = args.A + ((int64_t)bh * R + a) * R;
-  for (int i = threadIdx.x; i < R; i += 256) {
-    double p1 = exp(s1[i] - m1) / z1, p2 = exp(s2[i] - m2) / z2;
+  float* out = args.A + row * R;
+  for (int i = lane; i < R; i += 64) {
+    const double p1 = exp(s1[i] - m1) / z1, p2 = exp(s2[i] - m2) / z2;
     out[i] = (float)((1.0 - lam) * p1 + lam * p2);
   }
 }
@@ -198,8 +201,9 @@ hipError_t launch_draft(const DraftArgs& args, hipStream_t stream) {
       hipLaunchKernelGGL((draft_pool_kernel<64, float>), pool_grid, dim3(256), 0, stream, args);
   }
   const int nt = (args.R + 63) / 64;
-  hipLaunchKernelGGL(draft_logits_kernel, dim3(nt, nt, BH), dim3(256), 0, stream, args);
-  hipLaunchKernelGGL(draft_softmax_kernel, dim3(args.R, BH), dim3(256), 0, stream, args);
+  hipLaunchKernelGGL(draft_logits_kernel, dim3(nt, nt, 2 * BH), dim3(256), 0, stream, args);
+  const int64_t rows = (int64_t)BH * args.R;
+  hipLaunchKernelGGL(draft_softmax_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, args);
   return hipGetLastError();
 }
 

@@ -34,7 +34,9 @@ int32_t derive(const da2_problem* p, Dims* o) {
   d.R = d.T * ((d.Hg + 7) / 8) * ((d.Wg + 7) / 8);
   d.Npad = 64 * d.R;
   d.BH = d.B * d.H;
-  if (d.R > 65535 || d.N > (1ll << 31) - 1 || d.BH * d.R > (1ll << 31) - 1) return DA2_ERR_INVALID_ARG;
+  // launch grids put R and 2*B*H in 16-bit grid dimensions
+  if (d.R > 65535 || d.BH > 32767 || d.N > (1ll << 31) - 1 || d.BH * d.R > (1ll << 31) - 1)
+    return DA2_ERR_INVALID_ARG;
   *o = d;
   return DA2_OK;
 }

@@ -81,6 +81,9 @@ def test_invalid_problems():
     assert L.da2_sizes(None, 0, ctypes.byref(s)) == _lib.DA2_ERR_INVALID_ARG
     # more than 65535 blocks
     assert L.da2_sizes(ctypes.byref(api.problem(1, 1, 64, 2000, 80, 80)), 0, ctypes.byref(s)) == _lib.DA2_ERR_INVALID_ARG
+    # more than 32767 heads in total
+    assert L.da2_sizes(ctypes.byref(api.problem(2, 16384, 64, 1, 8, 8)), 0, ctypes.byref(s)) == _lib.DA2_ERR_INVALID_ARG
+    assert L.da2_sizes(ctypes.byref(api.problem(1, 32767, 64, 1, 8, 8)), 0, ctypes.byref(s)) == _lib.DA2_OK
     n = 10
     buf = (ctypes.c_int32 * n)()
     assert L.da2_layout_build(ctypes.byref(api.problem(1, 1, 64, 1, 8, 8)), buf, n) == _lib.DA2_ERR_INVALID_ARG
