@@ -11,9 +11,16 @@ whole step, 4*B*H*N^2*d flops per step; mixed_attn alone is reported too.
 The roofline object covers mixed_attn, the dominant kernel: algorithmic
 flops = retained tiles x 4*64*64*d (8-bit tiles priced at the int8/fp8
 peak, 4-bit tiles at the fp16 peak the NVFP4 path issues), divided by the
-kernel's average duration measured with HIP events on its stream.
+kernel's average duration measured with HIP events on its stream. Its
+``traffic`` is the HBM bytes per launch that rocprofv3 counted for the same
+kernel source (profiles/mixed_attn_traffic.json, FETCH_SIZE and WRITE_SIZE
+scaled by a plain-copy calibration), or null when the source has changed
+since. The ``hbm`` object rates draft_map and prep_operands against HBM
+bandwidth with the bytes each call must move: draft_map reads Q and K and
+writes A; prep_operands reads Q, K and V and writes the operand buffer.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -27,6 +34,29 @@ sys.path.insert(0, ROOT)
 PEAK_8BIT = 5.0e15      # MI355X dense int8 / fp8 MFMA (published)
 PEAK_FP16 = 2.5e15      # MI355X dense fp16 / bf16 MFMA (published)
 PEAK_HBM = 8.0e12       # bytes/s
+TRAFFIC = os.path.join(ROOT, "profiles", "mixed_attn_traffic.json")
+ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_32628_amd", "csrc", f) for f in ("attn.hip", "common.hpp", "launch.hpp")]
+
+
+def attn_source_hash():
+    h = hashlib.sha256()
+    for f in ATTN_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload):
+    """HBM bytes per mixed_attn launch recorded for this kernel source and
+    workload, or None."""
+    try:
+        with open(TRAFFIC) as fh:
+            rec = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != attn_source_hash() or rec.get("workload") != workload:
+        return None
+    return rec.get("read_bytes", 0) + rec.get("write_bytes", 0)
 
 
 def parse():
@@ -50,7 +80,7 @@ def cpu_baseline(w, Q, K, V):
     slot2tok, n_a, _ = partition.tile_partition(w.T, w.Hg, w.Wg)
     R = n_a.size
     rng = np.random.default_rng(0)
-    rows = sorted(rng.choice(R, 32, replace=False))
+    rows = sorted(rng.choice(R, min(R, 288), replace=False))
     q, k, v = Q[0, 0], K[0, 0], V[0, 0]
     t0 = time.perf_counter()
     A32, _ = draft.draft_head(q, k, slot2tok, n_a, w.lam)
@@ -140,6 +170,18 @@ def main():
     achieved = (F8 + F4) / t_attn
     peak_eff = (F8 + F4) / (F8 / PEAK_8BIT + F4 / PEAK_FP16)
     dense_flops = 4.0 * w.B * w.H * w.N ** 2 * w.d
+    # bytes each preparation call must move (bf16 inputs)
+    sizes = buf.sizes
+    e_in = w.B * w.H * w.N * w.d * 2
+    draft_bytes = 2 * e_in + sizes["A_bytes"]
+    prep_bytes = 3 * e_in + sizes["ops_bytes"]
+    t_draft, t_prep = stage_ms["draft_map"] * 1e-3, stage_ms["prep_operands"] * 1e-3
+    hbm = {"draft_map": {"bytes": draft_bytes, "GB/s": draft_bytes / t_draft / 1e9,
+                         "frac": draft_bytes / t_draft / PEAK_HBM},
+           "prep_operands": {"bytes": prep_bytes, "GB/s": prep_bytes / t_prep / 1e9,
+                             "frac": prep_bytes / t_prep / PEAK_HBM},
+           "combined_frac": (draft_bytes + prep_bytes) / (t_draft + t_prep) / PEAK_HBM,
+           "peak_GB/s": PEAK_HBM / 1e9}
     rec = {
         "metric": "mixed_attn ms + dense-equiv TFLOP/s @32760 tok×12 heads, % MFMA roofline",
         "value": dense_flops / (ms_step * 1e-3) / 1e12,
@@ -158,10 +200,12 @@ def main():
         "mixed_attn_dense_equiv_tflops": dense_flops / t_attn / 1e12,
         "tiles": {"8bit": n8, "4bit": n4},
         "roofline": {"bound": "mfma", "kernel": "mixed_attn_kernel", "achieved": achieved / 1e12,
-                     "peak": peak_eff / 1e12, "unit": "TFLOP/s", "frac": achieved / peak_eff, "traffic": None,
+                     "peak": peak_eff / 1e12, "unit": "TFLOP/s", "frac": achieved / peak_eff,
+                     "traffic": recorded_traffic(w.name),
                      "peak_note": "budget-weighted: 8-bit tiles at 5.0 PF (int8/fp8), 4-bit tiles at 2.5 PF "
                                   "(fp16 MFMA on exact NVFP4 reconstructions)",
                      "frac_vs_fp4_peak": achieved * (F8 / PEAK_8BIT + F4 / 10.0e15) / (F8 + F4)},
+        "hbm": hbm,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, Q, K, V)
