@@ -23,6 +23,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -39,10 +40,15 @@ ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_32628_amd", "csrc", f) for f in (
 
 
 def attn_source_hash():
+    """SHA-256 of the attention kernel's sources without comments and blank
+    lines (a comment edit does not change the kernel)."""
     h = hashlib.sha256()
     for f in ATTN_SOURCES:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f) as fh:
+            for line in fh:
+                code = re.sub(r"//.*", "", line).strip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()
 
 

@@ -1,10 +1,10 @@
 // Phased mixed-precision attention (phased-execution appendix; precision-state-
 // conversion equation; NVFP4 probability equation; INT8 paragraph).
 //
-// One wavefront owns one query block a (64 query slots = two 32-query tiles qt)
-// and walks its retained key blocks: the NVFP4 ones in ascending order, then the
-// INT8 ones. All blocks share the fp32 running maxima m, the denominators l and
-// the numerator U.
+// One workgroup of two waves owns one query block a (64 query slots); wave w
+// owns the 32-query tile qt = w. The workgroup walks the block's retained key
+// blocks: the NVFP4 ones in ascending order, then the INT8 ones. All blocks
+// share the fp32 running maxima m, the denominators l and the numerator U.
 //
 // Tiles use 32x32 MFMAs with the transposed products
 //     S^T = K Q^T      (rows = key slots, cols = queries)
@@ -21,10 +21,10 @@
 // units U_c / (eta delta_c), l / eta; the 8-bit phase accumulates amplified
 // weights 2^(z - m + 8.807) and E4M3 codes; Exit converts back.
 //
-// Latency: each block's V fragments are requested before its QK^T product and
-// the next block's K fragments right after it, so both loads are in flight
-// while the softmax runs. The query fragments sit in LDS (read once per block)
-// to leave registers for these prefetches.
+// Data movement: the K and V tiles of a key block are copied into LDS once per
+// workgroup (each wave copies half) and read by both waves; the loop is
+// software-pipelined by one block (see phase_loop), and the query fragments
+// of the wave's tile stay in registers for the whole phase.
 //
 // Weight conversions use the gfx950 instructions v_cvt_pk_fp8_f32 (E4M3) and
 // v_cvt_scalef32_pk_fp4_f32 / v_cvt_scalef32_pk_f16_fp4 (E2M1 and back, unit
