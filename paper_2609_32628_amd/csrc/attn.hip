@@ -229,16 +229,18 @@ __device__ inline void after(const T& v) {
 // workgroup's two waves own the query tiles qt = 0, 1 of the query block; the
 // key and value tiles of each key block are copied into LDS once (each wave
 // issues half of the fragments) and read by both waves. Iteration i:
-//   wait K(i+1) -> barrier -> S' = K(i+1) Q^T interleaved with the softmax of S
-//   -> barrier -> DMA K(i+2) -> wait V(i) -> barrier -> U += V(i)^T P^T
-//   -> barrier -> DMA V(i+1)
+//   wait K(i+1) -> barrier -> S' = K(i+1) Q^T interleaved with the first part
+//   of the softmax of S -> barrier -> DMA K(i+2) -> rest of the softmax
+//   -> wait V(i) -> barrier -> U += V(i)^T P^T -> barrier -> DMA V(i+1)
 // Frag: fragment type; NFK: fragments per K (and V) tile; SA: logit tile type.
-// first(S): logits of the first block. step<MASK>(S, S', nb, dk): the
-// interleaved region (MASK: block i is partial). pv(): the value product.
-template <int NFK, typename Frag, typename SA, typename FIRST, typename STEP, typename PV>
+// first(S): logits of the first block. region1<MASK>(S, S', nb, dk): the
+// logit MFMAs of block i+1 interleaved with the first part of the softmax of
+// block i (MASK: block i is partial); region2(S): the rest of the softmax, after
+// sK has been handed to the next copy. pv(): the value product.
+template <int NFK, typename Frag, typename SA, typename FIRST, typename STEP1, typename STEP2, typename PV>
 __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_a, const float* dKh,
                                   const Frag* Kh, const Frag* Vh, Frag* sK, Frag* sV, int wave, int lane,
-                                  FIRST first_qk, STEP region, PV pv) {
+                                  FIRST first_qk, STEP1 region1, STEP2 region2, PV pv) {
   constexpr int TILE = NFK * 64;  // fragments per tile
   constexpr int HALF = NFK / 2;   // fragments each wave copies
   auto dma_tile = [&](const Frag* src, Frag* dst) {
@@ -277,17 +279,17 @@ __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_
     wait_vmem_keep<HALF>();
     wg_barrier();
     if (nb < kCap)
-      region.template operator()<true>(Sc, Sn, nb, dk);
+      region1.template operator()<true>(Sc, Sn, nb, dk);
     else
-      region.template operator()<false>(Sc, Sn, nb, dk);
+      region1.template operator()<false>(Sc, Sn, nb, dk);
     wait_lds();
     wg_barrier();  // both waves are done with sK
-    if (more2) {
-      dma_tile(Kh + (int64_t)kb2 * TILE, sK);
+    if (more2) dma_tile(Kh + (int64_t)kb2 * TILE, sK);
+    region2(Sc);  // returns after its results exist, so the wait below stays after it
+    if (more2)
       wait_vmem_keep<HALF>();  // V(i) copied, K(i+2) may still be in flight
-    } else {
+    else
       wait_vmem_keep<0>();
-    }
     wg_barrier();
     pv();
     wait_lds();
@@ -349,15 +351,16 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
         for (int j = 0; j < 2; ++j)
           S[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sK[(j * NS16 + s) * 64 + lane], Qf[s], S[j], 0, 0, 0);
     };
-    // Interleaved region: logits of the next block (NS16 stages of two
-    // MFMAs, operands read one stage ahead) with the softmax of the current
-    // one split into 8 pieces over the stages.
-    auto region = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float) {
+    // Softmax state of the current block, shared by the two regions.
+    float gm0 = 0.0f, gm1 = 0.0f, mn = 0.0f;
+    Fp4Group G0, G1;
+    // Region 1: logits of the next block (NS16 stages of two MFMAs, operands
+    // read one stage ahead) with the row maxima and the first group's
+    // exponentials of the current block in five pieces over the stages.
+    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float) {
       if constexpr (MASK) mask_tail(Sc, nb, g);
-      float gm0 = 0.0f, gm1 = 0.0f, mn = 0.0f;
-      Fp4Group G0, G1;
       f16x8 k0 = sK[lane], k1 = sK[NS16 * 64 + lane];
-      constexpr int PPS = 8 / NS16;  // softmax pieces per stage
+      constexpr int NP = 5;
 #pragma unroll
       for (int s = 0; s < NS16; ++s) {
         f16x8 n0 = k0, n1 = k1;
@@ -368,8 +371,8 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
         Sn[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(k0, Qf[s], s == 0 ? f32x16{} : Sn[0], 0, 0, 0);
         Sn[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(k1, Qf[s], s == 0 ? f32x16{} : Sn[1], 0, 0, 0);
 #pragma unroll
-        for (int q = 0; q < PPS; ++q) {
-          const int piece = s * PPS + q;
+        for (int piece = 0; piece < NP; ++piece) {
+          if (piece * NS16 / NP != s) continue;
           if (piece == 0) {
             gm0 = max16(Sc[0]);
           } else if (piece == 1) {
@@ -377,24 +380,23 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
             mn = new_max(fmaxf(gm0, gm1), c4, m, l, alpha);
           } else if (piece == 2) {
             fp4_setup(G0, gm0, c4, mn);
-            fp4_exps<0, 4>(G0, Sc[0], c4);
+            fp4_exps<0, 5>(G0, Sc[0], c4);
           } else if (piece == 3) {
-            fp4_exps<4, 10>(G0, Sc[0], c4);
-          } else if (piece == 4) {
-            fp4_exps<10, 16>(G0, Sc[0], c4);
-          } else if (piece == 5) {
-            fp4_pack(G0, P[0], P[1]);
-            fp4_setup(G1, gm1, c4, mn);
-          } else if (piece == 6) {
-            fp4_exps<0, 8>(G1, Sc[1], c4);
+            fp4_exps<5, 10>(G0, Sc[0], c4);
           } else {
-            fp4_exps<8, 16>(G1, Sc[1], c4);
+            fp4_exps<10, 16>(G0, Sc[0], c4);
           }
         }
         fence();
         k0 = n0;
         k1 = n1;
       }
+    };
+    // Region 2: the second group's weights and both groups' fp16 operands.
+    auto region2 = [&](SA& Sc) {
+      fp4_pack(G0, P[0], P[1]);
+      fp4_setup(G1, gm1, c4, mn);
+      fp4_exps<0, 16>(G1, Sc[1], c4);
       fp4_pack(G1, P[2], P[3]);
       l += weight_sum(G0) + weight_sum(G1);
       after(P[0]), after(P[1]), after(P[2]), after(P[3]), after(l);
@@ -420,7 +422,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
     };
     phase_loop<2 * NS16, f16x8, SA>(keys, n4, L.n_a, dKh, reinterpret_cast<const f16x8*>(args.K4) + blk0 * (kCap * D / 8),
                                  reinterpret_cast<const f16x8*>(args.V4) + blk0 * (kCap * D / 8), sK, sV, wave, lane,
-                                 qk, region, pv);
+                                 qk, region1, region2, pv);
   }
 
   // per-lane channel of accumulator register i of channel tile t
@@ -459,20 +461,21 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
         for (int j = 0; j < 2; ++j)
           S[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(sK8[(j * NS32 + s) * 64 + lane], Qf[s], S[j], 0, 0, 0);
     };
-    // Interleaved region: logits of the next block (NS32 stages of two int8
-    // MFMAs) with the softmax of the current one in 4 pieces.
-    auto region = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float dk) {
-      const float cb = c8a * dk;
-      f32x16 sf[2];
+    // Softmax state of the current block, shared by the two regions.
+    f32x16 sf[2];
+    float cb = 0.0f, off = 0.0f, s0 = 0.0f, s1 = 0.0f;
+    int w[8];
+    // Region 1: logits of the next block (NS32 stages of two int8 MFMAs) with
+    // the conversion, the row maxima and the first half of the weights.
+    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float dk) {
+      cb = c8a * dk;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int i = 0; i < 16; ++i) sf[j][i] = (float)Sc[j][i];
       if constexpr (MASK) mask_tail(sf, nb, g);
-      float off = 0.0f, s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
-      int w[8];
       i32x4 k0 = sK8[lane], k1 = sK8[NS32 * 64 + lane];
-      constexpr int PPS = 4 / NS32;
+      constexpr int NP = 2;
 #pragma unroll
       for (int s = 0; s < NS32; ++s) {
         i32x4 n0 = k0, n1 = k1;
@@ -483,22 +486,24 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
         Sn[0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(k0, Qf[s], s == 0 ? i32x16{} : Sn[0], 0, 0, 0);
         Sn[1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(k1, Qf[s], s == 0 ? i32x16{} : Sn[1], 0, 0, 0);
 #pragma unroll
-        for (int q = 0; q < PPS; ++q) {
-          const int piece = s * PPS + q;
+        for (int piece = 0; piece < NP; ++piece) {
+          if (piece * NS32 / NP != s) continue;
           if (piece == 0) {
             off = kExpOffset - new_max(fmaxf(max16(sf[0]), max16(sf[1])), cb, m, l, alpha);
-          } else if (piece == 1) {
+          } else {
             s0 = fp8_weights8<0>(sf[0], cb, off, w[0], w[1]);
             s1 = fp8_weights8<8>(sf[0], cb, off, w[2], w[3]);
-          } else if (piece == 2) {
-            s2 = fp8_weights8<0>(sf[1], cb, off, w[4], w[5]);
-            s3 = fp8_weights8<8>(sf[1], cb, off, w[6], w[7]);
           }
         }
         fence();
         k0 = n0;
         k1 = n1;
       }
+    };
+    // Region 2: the second half of the weights and the fp8 P^T operand.
+    auto region2 = [&](SA&) {
+      const float s2 = fp8_weights8<0>(sf[1], cb, off, w[4], w[5]);
+      const float s3 = fp8_weights8<8>(sf[1], cb, off, w[6], w[7]);
       P = i32x8{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]};
       l += (s0 + s1) + (s2 + s3);
       after(P), after(l);
@@ -524,7 +529,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
     phase_loop<2 * NS32, i32x4, SA>(keys + n4, n8, L.n_a, dKh,
                                  reinterpret_cast<const i32x4*>(args.K8) + blk0 * (kCap * D / 16),
                                  reinterpret_cast<const i32x4*>(args.V8) + blk0 * (kCap * D / 16), sK8, sV8, wave,
-                                 lane, qk, region, pv);
+                                 lane, qk, region1, region2, pv);
     // Exit: U_c <- eta delta_c U_c, l <- eta l
 #pragma unroll
     for (int t = 0; t < NT; ++t)
