@@ -2,15 +2,17 @@
 (oracle; test infrastructure).
 
 Paper: "Phased execution" and "Cross-precision accumulation" (retained key
-blocks of a query block are grouped into an NVFP4 segment followed by an
-INT8 segment; all blocks share the row maxima, the denominator and the
-output numerator; one normalization at the end), the NVFP4 probability
-equation, the INT8 paragraph of the format appendix, the
-precision-state-conversion equation (Enter / Exit), "Weight Quantization
-under Shared Normalization" and the reconstructed-output equation.
+blocks of a query block are grouped into an NVFP4 segment, an INT8 segment
+and a 16-bit segment, processed in that order; all blocks share the row
+maxima, the denominator and the output numerator; one normalization at the
+end), the NVFP4 probability equation, the INT8 and FP16 paragraph of the
+format appendix, the precision-state-conversion equation (Enter / Exit),
+the phased-execution appendix (the FP16 phase continues in the common
+scale), "Weight Quantization under Shared Normalization" and the
+reconstructed-output equation.
 
 For one query region a with retained key blocks L = [list4 ascending ;
-list8 ascending] and valid query u:
+list8 ascending ; list16 ascending] and valid query u:
 
   s_uv  = Qhat_u . Khat_v / sqrt(d)     (reconstructed operands, float64)
   m_j   = max(m_{j-1}, max_{v in block j} s_uv)        (running maximum)
@@ -18,6 +20,7 @@ list8 ascending] and valid query u:
   4-bit block: sigma_P = E4M3(448 max_{v in G} Pt_uv) over 16-slot groups,
                w_uv = sigma_P / 2688 * E2M1(2688 Pt_uv / sigma_P)
   8-bit block: w_uv = eta * E4M3(Pt_uv / eta), eta = 2^-8.807
+  16-bit block: w_uv = FP16(Pt_uv), Qhat, Khat, Vhat the FP16 values
   l = sum_j e^{m_j - m} sum_v Pt_uv,  U = sum_j e^{m_j - m} sum_v w_uv Vhat_v,
   O_u = U / l   (0 for a row with no retained block),  m = m_last.
 
@@ -29,7 +32,8 @@ is used to check the closed form.
 Readings: the running maximum is updated once per 64-slot key block; the
 denominator takes the float32-before-conversion weights (here exact);
 eta = 2^-8.807 exactly, the value the printed 0.0022326917 rounds; key
-blocks ascend within a phase; padded key slots carry no weight.
+blocks ascend within a phase; padded key slots carry no weight; the FP16
+weight is the round-to-nearest-even half-precision value of the exact Pt.
 """
 import numpy as np
 
@@ -57,6 +61,11 @@ def quant_weights_fp8(Pt):
     return ETA * e4m3(AMP * Pt)
 
 
+def quant_weights_fp16(Pt):
+    """16-bit path weights: Pt cast to IEEE half precision (round to nearest even)."""
+    return np.asarray(Pt, np.float64).astype(np.float16).astype(np.float64)
+
+
 def identity_weights(Pt):
     return Pt
 
@@ -64,7 +73,7 @@ def identity_weights(Pt):
 class Operands:
     """Per-phase reconstructed operands of one head, slot ordered [R, 64, d].
 
-    ``phases`` maps 4 and 8 to (Qhat, Khat, Vhat, weight_quantizer)."""
+    ``phases`` maps 4, 8 and 16 to (Qhat, Khat, Vhat, weight_quantizer)."""
 
     def __init__(self, n_a, phases):
         self.n_a = n_a
@@ -73,13 +82,15 @@ class Operands:
     @classmethod
     def quantized(cls, rec, n_a):
         return cls(n_a, {4: (rec["Qh4"], rec["Kh4"], rec["Vh4"], quant_weights_fp4),
-                         8: (rec["Qh8"], rec["Kh8"], rec["Vh8"], quant_weights_fp8)})
+                         8: (rec["Qh8"], rec["Kh8"], rec["Vh8"], quant_weights_fp8),
+                         16: (rec["Qh16"], rec["Kh16"], rec["Vh16"], quant_weights_fp16)})
 
     @classmethod
     def exact(cls, Qs, Ks, Vs, n_a):
         """No-quant mode: the original values on both paths, unquantized weights."""
         Q, K, V = (np.asarray(x, np.float64) for x in (Qs, Ks, Vs))
-        return cls(n_a, {4: (Q, K, V, identity_weights), 8: (Q, K, V, identity_weights)})
+        return cls(n_a, {4: (Q, K, V, identity_weights), 8: (Q, K, V, identity_weights),
+                         16: (Q, K, V, identity_weights)})
 
 
 def _segment(ops, a, blocks, phase):
@@ -93,11 +104,11 @@ def _segment(ops, a, blocks, phase):
     return S, Vh[blocks], quant
 
 
-def attend(ops, a, list4, list8, return_parts=False):
+def attend(ops, a, list4, list8, list16=(), return_parts=False):
     """Output rows [n_a[a], d] of query region a (closed form)."""
     nq = ops.n_a[a]
     d = ops.phases[4][0].shape[2]
-    segs = [(_segment(ops, a, lst, p), p) for lst, p in ((list4, 4), (list8, 8)) if len(lst)]
+    segs = [(_segment(ops, a, lst, p), p) for lst, p in ((list4, 4), (list8, 8), (list16, 16)) if len(lst)]
     if not segs:
         return np.zeros((nq, d))
     S = np.concatenate([s[0] for s, _ in segs], axis=1)                # [nq, nb, 64]
@@ -119,14 +130,15 @@ def attend(ops, a, list4, list8, return_parts=False):
     return O
 
 
-def attend_sequential(ops, a, list4, list8, dV, gV):
+def attend_sequential(ops, a, list4, list8, dV, gV, list16=()):
     """The online recurrence block by block, with the phase unit changes.
 
     Phase 4 accumulates U in units of g_V/2688 (its matrix products take
     sigma_P e_P and sigma_V e_V); Enter converts the state to the INT8
     path's units (U / (eta delta_c), l / eta); phase 8 accumulates the
     amplified weights Pt/eta and E4M3 codes times the E4M3 V codes; Exit
-    converts back (precision-state-conversion equation)."""
+    converts back (precision-state-conversion equation); phase 16 then
+    accumulates FP16 weights times FP16 values in the common units."""
     nq = ops.n_a[a]
     d = ops.phases[4][0].shape[2]
     dV = np.asarray(dV, np.float64)
@@ -161,7 +173,16 @@ def attend_sequential(ops, a, list4, list8, dV, gV):
             m = m_new
         U = U * (ETA * dV)[None, :]                                     # Exit
         ell = ell * ETA
-    if not (len(list4) or len(list8)):
+    for b in list16:
+        S, Vh, quant = _segment(ops, a, [b], 16)
+        S, Vh = S[:, 0], Vh[0]
+        m_new = np.maximum(m, S.max(axis=1))
+        alpha = np.exp(m - m_new)
+        Pt = np.exp(S - m_new[:, None])
+        ell = ell * alpha + Pt.sum(axis=1)
+        U = U * alpha[:, None] + quant(Pt) @ Vh
+        m = m_new
+    if not (len(list4) or len(list8) or len(list16)):
         return np.zeros((nq, d))
     return U / ell[:, None]
 
@@ -174,7 +195,7 @@ def dense_attention(Q, K, V):
     return (P / P.sum(axis=1, keepdims=True)) @ V
 
 
-def lemma_bound(ops, exact, a, list4, list8, Qtok, Ktok, Vtok, slot2tok):
+def lemma_bound(ops, exact, a, list4, list8, Qtok, Ktok, Vtok, slot2tok, list16=()):
     """Both sides of the block form of Lemma 3.2 for every valid query of region a.
 
     lhs_u = ||O_dense_u - Ohat_u||,
@@ -185,12 +206,12 @@ def lemma_bound(ops, exact, a, list4, list8, Qtok, Ktok, Vtok, slot2tok):
     nq = ops.n_a[a]
     Qtok, Ktok, Vtok = (np.asarray(x, np.float64) for x in (Qtok, Ktok, Vtok))
     d = Qtok.shape[1]
-    Oh, parts = attend(ops, a, list4, list8, return_parts=True)
+    Oh, parts = attend(ops, a, list4, list8, list16, return_parts=True)
     toks_q = slot2tok[a * CAP: a * CAP + nq]
     Od = dense_attention(Qtok[toks_q], Ktok, Vtok)
     lhs = np.linalg.norm(Od - Oh, axis=1)
     Vmax = np.linalg.norm(Vtok, axis=1).max()
-    blocks = list(list4) + list(list8)
+    blocks = list(list4) + list(list8) + list(list16)
     # exact logits of the retained blocks, same slot layout
     Se, _, _ = _segment(exact, a, blocks, 4)
     S, m, W, f = parts["S"], parts["m"], parts["W"], parts["f"]
@@ -203,8 +224,9 @@ def lemma_bound(ops, exact, a, list4, list8, Qtok, Ktok, Vtok, slot2tok):
     valid = np.isfinite(S)
     with np.errstate(invalid="ignore"):
         alpha_ub = np.where(valid, np.abs(S - Se), 0.0).max(axis=2)
-    Vh = np.concatenate([ops.phases[p][2][lst] for lst, p in ((list4, 4), (list8, 8)) if len(lst)])
-    Vx = np.concatenate([exact.phases[p][2][lst] for lst, p in ((list4, 4), (list8, 8)) if len(lst)])
+    segs = ((list4, 4), (list8, 8), (list16, 16))
+    Vh = np.concatenate([ops.phases[p][2][lst] for lst, p in segs if len(lst)])
+    Vx = np.concatenate([exact.phases[p][2][lst] for lst, p in segs if len(lst)])
     nu_b = np.linalg.norm(Vh - Vx, axis=2).max(axis=1)                  # [nb]
     nu_ub = np.broadcast_to(nu_b[None, :], m_ub.shape)
     omega_ub = np.abs(what - w).sum(axis=2) / np.maximum(w.sum(axis=2), 1e-300)

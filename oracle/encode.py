@@ -8,6 +8,8 @@ Paper: appendix "Quantization Formats and Scales".
 * E4M3 V (probability-value product of the INT8 path): per-channel scale
   delta_c = max_v |V_vc| / 2.25 over all valid keys of the head; all-zero
   channels encode to zero.
+* FP16 Q/K/V (16-bit path, INT8-and-FP16 paragraph): the values cast to
+  IEEE half precision, round to nearest even.
 * NVFP4 (NVFP4 quantization equation): E2M1 values with an E4M3 scale per
   group of 16 along the reduction dimension (channels for Q and K, key
   slots within a block for V), a positive per-tensor scale g_X,
@@ -86,13 +88,15 @@ def encode_head(Q, K, V, slot2tok, n_a, amaxQ=None, amaxK=None, amaxV=None):
       v8 E4M3 values [R,64,d]; dV float32 [d]
       gQ, gK, gV float32; sQ, sK E4M3 values [R,64,d/16]; eQ, eK [R,64,d];
       sV E4M3 values [R,4,d] (16-slot groups per channel); eV [R,64,d]
+      q16, k16, v16 float16 [R,64,d] (16-bit path)
     """
     Qs, Ks, Vs = (gather_slots(X.astype(np.float32), slot2tok) for X in (Q, K, V))
     R, _, d = Qs.shape
     q8, dQ = int8_blocks(Qs, n_a)
     k8, dK = int8_blocks(Ks, n_a)
     v8, dV = e4m3_values_per_channel(Vs, n_a)
-    out = dict(q8=q8, dQ=dQ, k8=k8, dK=dK, v8=v8, dV=dV)
+    out = dict(q8=q8, dQ=dQ, k8=k8, dK=dK, v8=v8, dV=dV,
+               q16=Qs.astype(np.float16), k16=Ks.astype(np.float16), v16=Vs.astype(np.float16))
     amaxes = {"Q": amaxQ, "K": amaxK, "V": amaxV}
     for name, Xs, X in (("Q", Qs, Q), ("K", Ks, K)):
         amax = amaxes[name] if amaxes[name] is not None else np.abs(X).max()
@@ -112,12 +116,16 @@ def encode_head(Q, K, V, slot2tok, n_a, amaxQ=None, amaxK=None, amaxV=None):
 def reconstruct(enc):
     """Operands in original units (float64), as the attention uses them.
 
-    Qh8/Kh8: delta * q; Vh8: delta_c * v8; Qh4/Kh4/Vh4: g * sigma * e."""
+    Qh8/Kh8: delta * q; Vh8: delta_c * v8; Qh4/Kh4/Vh4: g * sigma * e;
+    Qh16/Kh16/Vh16: the half-precision values."""
     R, _, d = enc["q8"].shape
     rec = {
         "Qh8": enc["q8"].astype(np.float64) * enc["dQ"].astype(np.float64)[:, None, None],
         "Kh8": enc["k8"].astype(np.float64) * enc["dK"].astype(np.float64)[:, None, None],
         "Vh8": enc["v8"] * enc["dV"].astype(np.float64)[None, None, :],
+        "Qh16": enc["q16"].astype(np.float64),
+        "Kh16": enc["k16"].astype(np.float64),
+        "Vh16": enc["v16"].astype(np.float64),
     }
     for name in ("Q", "K"):
         s = np.repeat(enc["s" + name], GROUP, axis=2)                   # [R,64,d]

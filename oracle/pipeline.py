@@ -9,15 +9,16 @@ import numpy as np
 from . import attention, draft, encode, partition, rank
 
 
-def run_head(Q, K, V, layout, lam, budgets, scope, rows=None, mode="quant"):
-    """One (batch, head). Q, K, V: [N, d] float32 values.
+def run_head(Q, K, V, layout, lam, budgets, scope, rows=None, mode="quant", num16=0):
+    """One (batch, head). Q, K, V: [N, d] float32 values; budgets
+    (num8, num4, den) plus num16/den for the 16-bit path.
 
     ``rows`` restricts the attention to a subset of query regions (the draft,
     ranking and encodings always cover the whole head). Returns a dict with
     A32, cls, enc, and O [N, d] float64 (rows not computed are NaN)."""
     slot2tok, n_a, _ = layout
     A32, pooled = draft.draft_head(Q, K, slot2tok, n_a, lam)
-    cls = rank.rank_head(A32, *budgets, scope)
+    cls = rank.rank_head(A32, *budgets, scope, num16=num16)
     enc = encode.encode_head(Q, K, V, slot2tok, n_a)
     if mode == "quant":
         ops = attention.Operands.quantized(encode.reconstruct(enc), n_a)
@@ -26,9 +27,9 @@ def run_head(Q, K, V, layout, lam, budgets, scope, rows=None, mode="quant"):
     R = n_a.size
     O = np.full(Q.shape, np.nan)
     for a in (range(R) if rows is None else rows):
-        l4, l8 = rank.key_lists(cls[a])
+        l4, l8, l16 = rank.key_lists_all(cls[a])
         toks = slot2tok[a * partition.CAP: a * partition.CAP + n_a[a]]
-        O[toks] = attention.attend(ops, a, l4, l8)
+        O[toks] = attention.attend(ops, a, l4, l8, l16)
     return dict(A32=A32, pooled=pooled, cls=cls, enc=enc, O=O)
 
 
@@ -39,5 +40,5 @@ def run(w, Q, K, V, heads=None, rows=None, mode="quant"):
     for b in range(Q.shape[0]):
         for h in (range(Q.shape[1]) if heads is None else heads):
             out.append(run_head(Q[b, h], K[b, h], V[b, h], layout, w.lam, w.budgets,
-                                w.scope, rows=rows, mode=mode))
+                                w.scope, rows=rows, mode=mode, num16=w.num16))
     return layout, out

@@ -7,8 +7,8 @@ Each workload is a synthetic stand-in for one video-DiT attention layer
 (the paper measures on captured HunyuanVideo / MiniMax-H3 activations,
 which are not available). Budgets are integer fractions
 ``(num8, num4, den)``: ``num8/den`` of the region pairs go to the 8-bit
-path, ``num4/den`` to the 4-bit path and the rest are skipped (Alg. 1
-with no 16-bit quota).
+path, ``num4/den`` to the 4-bit path and the rest are skipped; ``num16/den``
+(default 0, as on the hot path) go to the 16-bit path ahead of both (Alg. 1).
 """
 from dataclasses import dataclass, field, replace
 from typing import Tuple
@@ -31,6 +31,7 @@ class Workload:
     phase_drift: bool = False       # sinusoid phases drift across frames
     lam: float = 0.2                # pooling weight lambda of the draft map
     seed: int = 0
+    num16: int = 0                  # num16/den of the pairs go to the 16-bit path
 
     @property
     def N(self) -> int:

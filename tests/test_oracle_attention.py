@@ -188,3 +188,63 @@ def test_precision_ordering_of_error():
         err[name] = np.sqrt(num / den)
     assert err["8"] < err["mix"] < err["4"]
     assert err["8"] < 0.05 and err["4"] < 0.3
+
+
+def test_noquant_dense_equivalence_with_sixteen_bit_segment():
+    """No-quant mode: any split of all blocks over the three phases, including
+    the 16-bit one, is textbook dense attention."""
+    Q, K, V, layout = _case(8)
+    ops = _exact_ops(Q, K, V, layout)
+    R = layout[1].size
+    Od = att.dense_attention(Q, K, V)
+    for a in range(R):
+        b = np.arange(R)
+        for split in ((b, [], []), ([], [], b), (b[0::3], b[1::3], b[2::3])):
+            O = att.attend(ops, a, *split)
+            np.testing.assert_allclose(O, Od[_rows(layout, a)], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("lists", [([0, 2], [1], [3, 5]), ([], [], [0, 1, 4]), ([1], [], [2]), ([], [3], [0])])
+def test_closed_form_equals_sequential_three_phases(lists):
+    """The closed form equals the block recurrence whose 16-bit phase follows
+    the INT8 Exit (or the NVFP4 phase) in the common units."""
+    Q, K, V, layout = _case(9, scale=1.5)
+    enc, ops = _quant_ops(Q, K, V, layout)
+    l4, l8, l16 = lists
+    for a in range(layout[1].size):
+        O1 = att.attend(ops, a, l4, l8, l16)
+        O2 = att.attend_sequential(ops, a, l4, l8, enc["dV"], float(enc["gV"]), l16)
+        np.testing.assert_allclose(O1, O2, rtol=1e-12, atol=1e-13)
+
+
+def test_sixteen_bit_only_is_dense_on_half_operands_within_weight_rounding():
+    """All blocks on the 16-bit path: the output is dense attention over the
+    half-precision Q, K, V except that the numerator uses half-precision
+    weights. Each normal half weight is within 2^-11 of its value relative,
+    a subnormal one within 2^-25 absolute, and the denominator is at least 1
+    (the weight of the final maximum), so |O - O_dense16| <= (2^-11 +
+    n_keys 2^-25) max|V|."""
+    Q, K, V, layout = _case(10, scale=1.2)
+    slot2tok, n_a, _ = layout
+    enc, ops = _quant_ops(Q, K, V, layout)
+    Q16, K16, V16 = (X.astype(np.float16).astype(np.float64) for X in (Q, K, V))
+    Od = att.dense_attention(Q16, K16, V16)
+    R = n_a.size
+    bound = (2.0 ** -11 + K.shape[0] * 2.0 ** -25) * np.abs(V16).max()
+    worst = 0.0
+    for a in range(R):
+        O = att.attend(ops, a, [], [], np.arange(R))
+        err = np.abs(O - Od[_rows(layout, a)]).max()
+        worst = max(worst, err)
+        assert err <= bound, (a, err, bound)
+    assert worst > 0          # the weight rounding is really applied
+
+
+def test_fp16_weights_scalar():
+    """The 16-bit path's weight is the nearest half (ties to even), checked
+    with Python's own IEEE half packing."""
+    rng = np.random.default_rng(12)
+    Pt = np.concatenate([np.exp(-rng.exponential(4.0, 500)), [1.0, 2.0 ** -24, 3 * 2.0 ** -26, 1 + 2.0 ** -11]])
+    W = att.quant_weights_fp16(Pt)
+    for p, w in zip(Pt, W):
+        assert w == struct.unpack("e", struct.pack("e", float(p)))[0]

@@ -139,3 +139,21 @@ def test_padding_encodes_to_zero():
     for a in np.nonzero(n_a < 64)[0]:
         for key in ("q8", "k8", "v8", "eQ", "eK", "eV"):
             assert np.all(enc[key][a, n_a[a]:] == 0)
+
+
+def test_fp16_operands_are_half_casts():
+    """16-bit path operands: the slot-ordered values cast to IEEE half
+    (checked with Python's half packing); padding slots are zero."""
+    X, layout = _tiny(4)
+    slot2tok, n_a, _ = layout
+    enc = encode.encode_head(X, X, X, slot2tok, n_a)
+    Xs = partition.gather_slots(X, slot2tok)
+    for key in ("q16", "k16", "v16"):
+        got = enc[key].astype(np.float64)
+        assert got.dtype == np.float64 and enc[key].dtype == np.float16
+        for idx in zip(*np.nonzero(np.ones(Xs.shape[:2], bool))):
+            row = Xs[idx]
+            want = [struct.unpack("e", struct.pack("e", float(v)))[0] for v in row[:4]]
+            assert list(got[idx][:4]) == want
+        pad = np.arange(64)[None, :] >= n_a[:, None]
+        assert np.all(got[pad] == 0)
