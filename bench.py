@@ -132,8 +132,9 @@ def main():
 
     def step(ev=None):
         calls = (lambda: api.da2_draft_map(dev[0], dev[1], buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft),
-                 lambda: api.da2_rank_assign(buf.A, p, *w.budgets, w.scope, buf.cls, buf.lists, buf.ws_rank),
-                 lambda: api.da2_prep_operands(dev[0], dev[1], dev[2], buf.layout, p, buf.stats, buf.ops, None),
+                 lambda: api.da2_rank_assign(buf.A, p, w.num16, *w.budgets, w.scope, buf.cls, buf.lists, buf.ws_rank),
+                 lambda: api.da2_prep_operands(dev[0], dev[1], dev[2], buf.layout, p, int(w.num16 > 0), buf.stats,
+                                               buf.ops, None),
                  lambda: api.da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O))
         for i, c in enumerate(calls):
             if ev is not None:

@@ -6,7 +6,7 @@
  * all asynchronous on a caller-given HIP stream:
  *
  *   da2_draft_map      pooled draft attention map            (descriptor eq., Def. 3.1)
- *   da2_rank_assign    shared ranking into 8-bit/4-bit/skip  (Algorithm 1, routing appendix)
+ *   da2_rank_assign    shared ranking into 16/8/4-bit or skip (Algorithm 1, routing appendix)
  *   da2_prep_operands  per-block INT8 / E4M3 / NVFP4 operands (format appendix, NVFP4 eqs.)
  *   da2_mixed_attn     one phased mixed-precision attention   (phased execution,
  *                      kernel with shared softmax state       precision-state-conversion eq.)
@@ -119,26 +119,29 @@ int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const 
  * (float64 [B,H,R,d] each), [4] S_avg, [5] S_max (float64 [B,H,R,R] logits). */
 int32_t da2_ws_draft_offsets(const da2_problem* p, int64_t* offsets6);
 
-/* Shared ranking (Algorithm 1 without the 16-bit quota; routing appendix).
- * Quotas from budgets num8/den and num4/den over M = R*R pairs per head
- * (DA2_SCOPE_HEAD) or M = R pairs per query block (DA2_SCOPE_ROW):
- *   T8 = floor(num8*M/den + 1/2), T4 = floor((num8+num4)*M/den + 1/2) - T8.
+/* Shared ranking (Algorithm 1; routing appendix). Quotas from budgets
+ * num16/den, num8/den and num4/den over M = R*R pairs per head
+ * (DA2_SCOPE_HEAD) or M = R pairs per query block (DA2_SCOPE_ROW), cumulative
+ * and rounded half up: with h(n) = floor(n*M/den + 1/2),
+ *   T16 = h(num16), T8 = h(num16+num8) - T16, T4 = h(num16+num8+num4) - T16 - T8.
  * Pairs are ranked by (A descending, pair index ascending) with pair index
- * a*R+b (head) or b (row); ranks [0,T8) -> 8, [T8,T8+T4) -> 4, others -> 0.
+ * a*R+b (head) or b (row); ranks [0,T16) -> 16, the next T8 -> 8, the next
+ * T4 -> 4, others -> 0. The hot path runs with num16 = 0.
  *   A      device float32 [B,H,R,R] (e.g. from da2_draft_map)
- *   cls    device out, uint8 [B,H,R,R] in {0,4,8}
+ *   cls    device out, uint8 [B,H,R,R] in {0,4,8,16}
  *   lists  device out, lists_bytes (see da2_lists_offsets)
- * Errors: INVALID_ARG if den <= 0, num8 < 0, num4 < 0, num8+num4 > den, or
- * head scope with R*R >= 2^22. */
-int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num8, int32_t num4,
-                        int32_t den, int32_t scope, uint8_t* cls, void* lists, void* ws,
-                        int64_t ws_bytes, void* stream);
+ * Errors: INVALID_ARG if den <= 0, a budget < 0, num16+num8+num4 > den, or
+ * head scope with R*R >= 2^22; UNSUPPORTED for row scope with R > 8192. */
+int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int32_t num8,
+                        int32_t num4, int32_t den, int32_t scope, uint8_t* cls, void* lists,
+                        void* ws, int64_t ws_bytes, void* stream);
 
 /* Offsets (bytes) inside lists:
  *   [0] keys   uint16 [B*H*R][R]: row (b,h,a) holds its 4-bit key blocks
  *              ascending in [0,n4), then its 8-bit key blocks ascending in
- *              [n4, n4+n8)
- *   [1] counts int32 [B*H*R][2] = (n4, n8)
+ *              [n4, n4+n8), then its 16-bit key blocks ascending in
+ *              [n4+n8, n4+n8+n16)
+ *   [1] counts int32 [B*H*R][4] = (n4, n8, n16, 0)
  *   [2] order  int32 [B*H*R]: the work order of the rows (b*H+h)*R+a: grouped
  *              by head and by row parity, most expensive first in each group;
  *              attention workgroup w takes order[(w mod 8)*ceil(n/8) + w div 8]
@@ -157,13 +160,17 @@ int32_t da2_lists_offsets(const da2_problem* p, int64_t* offsets4);
  *     zeros. Stored as the exact fp16 value sigma*e (gfx950 has no MFMA that
  *     applies E4M3 scales per 16 elements; sigma*e has at most 6 significant
  *     bits, so fp16 holds it exactly and fp16 MFMA reproduces the products).
+ *   FP16 Q, K, V (16-bit path, INT8 and FP16 paragraph): the values rounded
+ *     to nearest-even half precision; written only when with16 = 1.
  * Casts round to nearest even and saturate; padding slots encode to zero.
  *   Q, K, V  device [B,H,N,d] per *qkv; stats from da2_draft_map (this call
  *            fills entries 2.. : max|V| and the per-channel max|V_c|)
+ *   with16   0 or 1: also write the 16-bit sections [10..12] of ops. A
+ *            da2_mixed_attn call whose lists hold 16-bit blocks needs them.
  *   ops      device out, ops_bytes (see da2_ops_offsets)                   */
 int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv,
-                          const int32_t* layout, const da2_problem* p, void* stats, void* ops,
-                          void* ws, int64_t ws_bytes, void* stream);
+                          const int32_t* layout, const da2_problem* p, int32_t with16, void* stats,
+                          void* ops, void* ws, int64_t ws_bytes, void* stream);
 
 /* Offsets (bytes) inside ops, per section; each section is [B*H][R][...]
  * with one 64-slot block per R, in the fragment order of the gfx950 MFMA
@@ -178,22 +185,27 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
  *   [7] dK  float32 [B*H][R]   INT8 scale of each key block
  *   [8] dV  float32 [B*H][d]   E4M3 per-channel scale of V
  *   [9] g   float32 [B*H][4]   (g_Q, g_K, g_V, 0) NVFP4 tensor scales
+ *   [10] Q16, [11] K16, [12] V16  fp16, the layouts of Q4, K4, V4 holding the
+ *            half-precision values of the 16-bit path
  * with kappa(j, r) = 32j + 16((r/4)%2) + 4(r/8) + r%4 (the key permutation
  * that puts each 16-slot group of a query row into one lane, see the operand
  * permutation equation). */
-int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets10);
+int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets13);
 
 /* Phased mixed-precision attention (phased-execution appendix;
- * precision-state-conversion equation). For each query block a (one wave,
- * 64 query slots) the NVFP4 key blocks are processed in ascending order, then
- * the INT8 ones, sharing fp32 row maxima m, denominator l and numerator U:
+ * precision-state-conversion equation). For each query block a (one
+ * workgroup, 64 query slots) the NVFP4 key blocks are processed in ascending
+ * order, then the INT8 ones, then the 16-bit ones, sharing fp32 row maxima m,
+ * denominator l and numerator U:
  *   s = Qhat Khat^T / sqrt d; m_j = max(m_{j-1}, rowmax_j s); Pt = exp(s - m_j)
  *   4-bit: l += sum Pt; sigma_P = E4M3(448 max_16 Pt); U += (sigma_P/2688)
  *          E2M1(2688 Pt/sigma_P) Vhat4 (fp16 MFMA on sigma*e operands)
  *   Enter: U_c /= eta delta_c, l /= eta   (eta = 2^-8.807)
  *   8-bit: int8 MFMA logits; P = 2^((s - m) log2 e + 8.807); l += sum P;
  *          U += E4M3(P) V8 (fp8 MFMA)
- *   Exit:  U_c *= eta delta_c, l *= eta;  O = U / l (0 if no retained block)
+ *   Exit:  U_c *= eta delta_c, l *= eta
+ *   16-bit: fp16 MFMA logits; Pt = exp(s - m); l += sum Pt; U += fp16(Pt) V16
+ *   O = U / l (0 if no retained block)
  * and the rows are written to token order through slot2tok.
  *   ops, lists, layout  device, from the calls above
  *   out      descriptor of O (dtype fp32 or bf16)

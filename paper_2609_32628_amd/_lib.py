@@ -62,9 +62,9 @@ def lib():
             "da2_layout_build": (i32, [P, pi32, i64]),
             "da2_draft_map": (i32, [vp, vp, T, vp, P, dbl, vp, vp, vp, i64, vp]),
             "da2_ws_draft_offsets": (i32, [P, pi64]),
-            "da2_rank_assign": (i32, [vp, P, i32, i32, i32, i32, vp, vp, vp, i64, vp]),
+            "da2_rank_assign": (i32, [vp, P, i32, i32, i32, i32, i32, vp, vp, vp, i64, vp]),
             "da2_lists_offsets": (i32, [P, pi64]),
-            "da2_prep_operands": (i32, [vp, vp, vp, T, vp, P, vp, vp, vp, i64, vp]),
+            "da2_prep_operands": (i32, [vp, vp, vp, T, vp, P, i32, vp, vp, vp, i64, vp]),
             "da2_ops_offsets": (i32, [P, pi64]),
             "da2_mixed_attn": (i32, [vp, vp, vp, P, T, vp, vp]),
         }

@@ -69,7 +69,7 @@ def da2_lists_offsets(p):
 
 
 def da2_ops_offsets(p):
-    return _offsets("da2_ops_offsets", p, 10)
+    return _offsets("da2_ops_offsets", p, 13)
 
 
 def da2_draft_map(Q, K, layout, p, lam, A, stats, ws, stream=None):
@@ -78,19 +78,19 @@ def da2_draft_map(Q, K, layout, p, lam, A, stats, ws, stream=None):
         _ptr(A), _ptr(stats), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def da2_rank_assign(A, p, num8, num4, den, scope, cls, lists, ws, stream=None):
+def da2_rank_assign(A, p, num16, num8, num4, den, scope, cls, lists, ws, stream=None):
     check("da2_rank_assign", lib().da2_rank_assign(
-        _ptr(A), ctypes.byref(p), num8, num4, den, SCOPES[scope], _ptr(cls), _ptr(lists), _ptr(ws),
+        _ptr(A), ctypes.byref(p), num16, num8, num4, den, SCOPES[scope], _ptr(cls), _ptr(lists), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def da2_prep_operands(Q, K, V, layout, p, stats, ops, ws, stream=None):
+def da2_prep_operands(Q, K, V, layout, p, with16, stats, ops, ws, stream=None):
     if not (Q.shape == K.shape == V.shape and Q.stride() == K.stride() == V.stride() and Q.dtype == K.dtype == V.dtype):
         raise ValueError("Q, K and V must share shape, strides and dtype")
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     check("da2_prep_operands", lib().da2_prep_operands(
-        _ptr(Q), _ptr(K), _ptr(V), ctypes.byref(_tensor_desc(Q)), _ptr(layout), ctypes.byref(p), _ptr(stats),
-        _ptr(ops), None if ws is None else _ptr(ws), ws_bytes, _stream(stream)))
+        _ptr(Q), _ptr(K), _ptr(V), ctypes.byref(_tensor_desc(Q)), _ptr(layout), ctypes.byref(p), int(with16),
+        _ptr(stats), _ptr(ops), None if ws is None else _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def da2_mixed_attn(ops, lists, layout, p, O, stream=None):
@@ -131,11 +131,12 @@ def alloc(p, scope="head", device="cuda"):
                    ws_draft=raw(s["ws_draft_bytes"]), ws_rank=raw(s["ws_rank_bytes"]))
 
 
-def attention(Q, K, V, buf, lam, budgets, O, stream=None):
-    """The four calls in order: draft map, ranking, operand preparation, attention."""
+def attention(Q, K, V, buf, lam, budgets, O, stream=None, num16=0):
+    """The four calls in order: draft map, ranking, operand preparation,
+    attention. budgets = (num8, num4, den); num16/den go to the 16-bit path."""
     p = buf.p
     da2_draft_map(Q, K, buf.layout, p, lam, buf.A, buf.stats, buf.ws_draft, stream)
-    da2_rank_assign(buf.A, p, *budgets, buf.scope, buf.cls, buf.lists, buf.ws_rank, stream)
-    da2_prep_operands(Q, K, V, buf.layout, p, buf.stats, buf.ops, None, stream)
+    da2_rank_assign(buf.A, p, num16, *budgets, buf.scope, buf.cls, buf.lists, buf.ws_rank, stream)
+    da2_prep_operands(Q, K, V, buf.layout, p, int(num16 > 0), buf.stats, buf.ops, None, stream)
     da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, stream)
     return O

@@ -1,10 +1,11 @@
 // Phased mixed-precision attention (phased-execution appendix; precision-state-
-// conversion equation; NVFP4 probability equation; INT8 paragraph).
+// conversion equation; NVFP4 probability equation; INT8 and FP16 paragraph).
 //
 // One workgroup of two waves owns one query block a (64 query slots); wave w
 // owns the 32-query tile qt = w. The workgroup walks the block's retained key
-// blocks: the NVFP4 ones in ascending order, then the INT8 ones. All blocks
-// share the fp32 running maxima m, the denominators l and the numerator U.
+// blocks: the NVFP4 ones in ascending order, then the INT8 ones, then the
+// 16-bit ones. All blocks share the fp32 running maxima m, the denominators l
+// and the numerator U.
 //
 // Tiles use 32x32 MFMAs with the transposed products
 //     S^T = K Q^T      (rows = key slots, cols = queries)
@@ -19,7 +20,8 @@
 // Units: the 4-bit phase multiplies fp16 sigma*e operands, so U carries a factor
 // 2688/g_V and l the unamplified weights; Enter converts to the 8-bit path's
 // units U_c / (eta delta_c), l / eta; the 8-bit phase accumulates amplified
-// weights 2^(z - m + 8.807) and E4M3 codes; Exit converts back.
+// weights 2^(z - m + 8.807) and E4M3 codes; Exit converts back; the 16-bit
+// phase then accumulates fp16 weights times fp16 values in the common units.
 //
 // Data movement: the K and V tiles of a key block are copied into LDS once per
 // workgroup (each wave copies half) and read by both waves; the loop is
@@ -155,6 +157,20 @@ __device__ inline float fp8_weights8(const f32x16& S, float cb, float off, int& 
   w0 = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], 0, false), true);
   w1 = __builtin_amdgcn_cvt_pk_fp8_f32(p[6], p[7], __builtin_amdgcn_cvt_pk_fp8_f32(p[4], p[5], 0, false), true);
   return sum;
+}
+
+// 16-bit path weights of 8 logits S[I0..I0+8) of this lane: Pt = 2^(S c - mn)
+// in fp32 (added to sum) and rounded to nearest-even fp16 for the P^T operand.
+template <int I0>
+__device__ inline f16x8 half_weights8(const f32x16& S, float c, float mn, float& sum) {
+  f16x8 h;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float y = exp2_fast(__builtin_fmaf(S[I0 + e], c, -mn));
+    sum += y;
+    h[e] = (_Float16)y;
+  }
+  return h;
 }
 
 // Scheduling fence: no instruction moves across it, so the stages between two
@@ -321,7 +337,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
   const int item = args.order[idx];
   const int bh = item / R, a = item % R;
   const Layout L = layout_view(args.layout, R, args.Npad);
-  const int n4 = args.counts[2 * item], n8 = args.counts[2 * item + 1];
+  const int n4 = args.counts[4 * item], n8 = args.counts[4 * item + 1], n16 = args.counts[4 * item + 2];
   const uint16_t* keys = args.keys + (int64_t)item * R;
   const int64_t blk0 = (int64_t)bh * R;  // first block of this head
   const float* dKh = args.dK + blk0;
@@ -540,6 +556,97 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
     const float restore = gV / 2688.0f;
 #pragma unroll
     for (int t = 0; t < NT; ++t) U[t] *= restore;
+  }
+
+  // ------------------------------ 16-bit phase ------------------------------
+  // Continues in the common units: fp16 Q, K, V; Pt = 2^(s log2 e / sqrt d - m)
+  // in fp32 (denominator), rounded to fp16 for the value product.
+  if (n16 > 0) {
+    const float c16 = kLog2e * rsqd;
+    f16x8 Qf[NS16];
+    const f16x8* Qa = reinterpret_cast<const f16x8*>(args.Q16) + (blk0 + a) * (kCap * D / 8);
+#pragma unroll
+    for (int s = 0; s < NS16; ++s) Qf[s] = Qa[(qt * NS16 + s) * 64 + lane];
+    f16x8 P[4];
+    float alpha = 1.0f;
+    typedef f32x16 SA[2];
+    auto qk = [&](SA& S) {
+      S[0] = S[1] = f32x16{};
+#pragma unroll
+      for (int s = 0; s < NS16; ++s)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          S[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(sK[(j * NS16 + s) * 64 + lane], Qf[s], S[j], 0, 0, 0);
+    };
+    float gm0 = 0.0f, gm1 = 0.0f, mn = 0.0f, sum0 = 0.0f, sum1 = 0.0f;
+    // Region 1: logits of the next block with the maxima and the first
+    // group's weights of the current block (four pieces over the stages).
+    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float) {
+      if constexpr (MASK) mask_tail(Sc, nb, g);
+      f16x8 k0 = sK[lane], k1 = sK[NS16 * 64 + lane];
+      constexpr int NP = 4;
+      sum0 = 0.0f;
+#pragma unroll
+      for (int s = 0; s < NS16; ++s) {
+        f16x8 n0 = k0, n1 = k1;
+        if (s + 1 < NS16) {
+          n0 = sK[(s + 1) * 64 + lane];
+          n1 = sK[(NS16 + s + 1) * 64 + lane];
+        }
+        Sn[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(k0, Qf[s], s == 0 ? f32x16{} : Sn[0], 0, 0, 0);
+        Sn[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(k1, Qf[s], s == 0 ? f32x16{} : Sn[1], 0, 0, 0);
+#pragma unroll
+        for (int piece = 0; piece < NP; ++piece) {
+          if (piece * NS16 / NP != s) continue;
+          if (piece == 0) {
+            gm0 = max16(Sc[0]);
+          } else if (piece == 1) {
+            gm1 = max16(Sc[1]);
+            mn = new_max(fmaxf(gm0, gm1), c16, m, l, alpha);
+          } else if (piece == 2) {
+            P[0] = half_weights8<0>(Sc[0], c16, mn, sum0);
+          } else {
+            P[1] = half_weights8<8>(Sc[0], c16, mn, sum0);
+          }
+        }
+        fence();
+        k0 = n0;
+        k1 = n1;
+      }
+    };
+    // Region 2: the second group's weights.
+    auto region2 = [&](SA& Sc) {
+      sum1 = 0.0f;
+      P[2] = half_weights8<0>(Sc[1], c16, mn, sum1);
+      P[3] = half_weights8<8>(Sc[1], c16, mn, sum1);
+      l += sum0 + sum1;
+      after(P[0]), after(P[1]), after(P[2]), after(P[3]), after(l);
+    };
+    // U += V^T P^T; value fragments are read two MFMAs ahead.
+    auto pv = [&]() {
+      if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+      constexpr int NM = 4 * NT;
+      auto vfrag = [&](int k) { return sV[((k % NT) * 4 + k / NT) * 64 + lane]; };
+      f16x8 v0 = vfrag(0), v1 = vfrag(1);
+#pragma unroll
+      for (int k = 0; k < NM; ++k) {
+        const f16x8 cur = (k & 1) ? v1 : v0;
+        if (k + 2 < NM) {
+          if (k & 1)
+            v1 = vfrag(k + 2);
+          else
+            v0 = vfrag(k + 2);
+        }
+        U[k % NT] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur, P[k / NT], U[k % NT], 0, 0, 0);
+        fence();
+      }
+    };
+    wait_lds();
+    wg_barrier();  // the previous phase is done with sK / sV
+    phase_loop<2 * NS16, f16x8, SA>(keys + n4 + n8, n16, L.n_a, dKh,
+                                    reinterpret_cast<const f16x8*>(args.K16) + blk0 * (kCap * D / 8),
+                                    reinterpret_cast<const f16x8*>(args.V16) + blk0 * (kCap * D / 8), sK, sV, wave,
+                                    lane, qk, region1, region2, pv);
   }
 
   // ------------------------- normalize and scatter -------------------------

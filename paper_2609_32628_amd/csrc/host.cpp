@@ -49,22 +49,23 @@ void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
   s->A_bytes = 4 * d.BH * d.R * d.R;
   s->cls_bytes = d.BH * d.R * d.R;
   s->stats_bytes = 4 * d.BH * (4 + d.d);
-  s->lists_bytes = align_up(2 * d.BH * d.R * d.R) + align_up(8 * d.BH * d.R) + align_up(4 * d.BH * d.R) + kAlign;
+  s->lists_bytes = align_up(2 * d.BH * d.R * d.R) + align_up(16 * d.BH * d.R) + align_up(4 * d.BH * d.R) + kAlign;
   const int64_t e = d.BH * d.Npad * d.d;
   s->ops_bytes = 3 * align_up(2 * e) + 3 * align_up(e) + 2 * align_up(4 * d.BH * d.R) + align_up(4 * d.BH * d.d) +
-                 align_up(16 * d.BH);
+                 align_up(16 * d.BH) + 3 * align_up(2 * e);
   s->ws_draft_bytes = 4 * align_up(8 * d.BH * d.R * d.d) + 2 * align_up(8 * d.BH * d.R * d.R);
-  int64_t thr = scope == DA2_SCOPE_ROW ? 16 * d.BH * d.R : 16 * d.BH;
-  s->ws_rank_bytes = align_up(4 * d.BH * 2 * 2048) + align_up(thr) + align_up(16 * d.BH) + align_up(16 * d.BH) +
-                     align_up(4 * d.BH * d.R);
+  int64_t thr = scope == DA2_SCOPE_ROW ? 8 * da2::kCuts * d.BH * d.R : 8 * da2::kCuts * d.BH;
+  s->ws_rank_bytes = align_up(4 * d.BH * da2::kCuts * 2048) + align_up(thr) + align_up(8 * da2::kCuts * d.BH) +
+                     align_up(8 * da2::kCuts * d.BH) + align_up(4 * d.BH * d.R);
   s->ws_prep_bytes = 0;
 }
 
 void ops_offsets(const Dims& d, int64_t* off) {
   const int64_t e = d.BH * d.Npad * d.d;
   int64_t o = 0;
-  const int64_t sz[10] = {2 * e, 2 * e, 2 * e, e, e, e, 4 * d.BH * d.R, 4 * d.BH * d.R, 4 * d.BH * d.d, 16 * d.BH};
-  for (int i = 0; i < 10; ++i) {
+  const int64_t sz[13] = {2 * e, 2 * e, 2 * e, e, e, e, 4 * d.BH * d.R, 4 * d.BH * d.R, 4 * d.BH * d.d, 16 * d.BH,
+                          2 * e, 2 * e, 2 * e};
+  for (int i = 0; i < 13; ++i) {
     off[i] = o;
     o += align_up(sz[i]);
   }
@@ -73,7 +74,7 @@ void ops_offsets(const Dims& d, int64_t* off) {
 void lists_offsets(const Dims& d, int64_t* off) {
   off[0] = 0;
   off[1] = align_up(2 * d.BH * d.R * d.R);
-  off[2] = off[1] + align_up(8 * d.BH * d.R);
+  off[2] = off[1] + align_up(16 * d.BH * d.R);
   off[3] = off[2] + align_up(4 * d.BH * d.R);
 }
 
@@ -239,13 +240,15 @@ int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const 
   return hip_status(da2::launch_draft(a, static_cast<hipStream_t>(stream)));
 }
 
-int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num8, int32_t num4, int32_t den,
-                        int32_t scope, uint8_t* cls, void* lists, void* ws, int64_t ws_bytes, void* stream) {
+int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int32_t num8, int32_t num4,
+                        int32_t den, int32_t scope, uint8_t* cls, void* lists, void* ws, int64_t ws_bytes,
+                        void* stream) {
   Dims d;
   int32_t st = derive(p, &d);
   if (st) return st;
   if (!A || !cls || !lists || !ws) return DA2_ERR_INVALID_ARG;
-  if (den <= 0 || num8 < 0 || num4 < 0 || (int64_t)num8 + num4 > den) return DA2_ERR_INVALID_ARG;
+  if (den <= 0 || num16 < 0 || num8 < 0 || num4 < 0 || (int64_t)num16 + num8 + num4 > den)
+    return DA2_ERR_INVALID_ARG;
   if (scope != DA2_SCOPE_HEAD && scope != DA2_SCOPE_ROW) return DA2_ERR_INVALID_ARG;
   if (scope == DA2_SCOPE_HEAD && d.R * d.R >= (1ll << 22)) return DA2_ERR_INVALID_ARG;
   if (scope == DA2_SCOPE_ROW && d.R > 8192) return DA2_ERR_UNSUPPORTED;
@@ -254,21 +257,22 @@ int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num8, int3
   if (ws_bytes < sz.ws_rank_bytes) return DA2_ERR_WORKSPACE;
   if ((st = check_device())) return st;
   const int64_t M = scope == DA2_SCOPE_HEAD ? d.R * d.R : d.R;
-  const int64_t c8 = (2 * (int64_t)num8 * M + den) / (2 * (int64_t)den);
-  const int64_t c84 = (2 * ((int64_t)num8 + num4) * M + den) / (2 * (int64_t)den);
+  // cumulative quotas, rounded half up: ranks [0, cut0) -> 16, [cut0, cut1) -> 8, [cut1, cut2) -> 4
+  auto half_up = [&](int64_t num) { return (2 * num * M + den) / (2 * (int64_t)den); };
   int64_t lo[4];
   lists_offsets(d, lo);
   char* lb = static_cast<char*>(lists);
   char* w = static_cast<char*>(ws);
-  int64_t thr = scope == DA2_SCOPE_ROW ? 16 * d.BH * d.R : 16 * d.BH;
+  int64_t thr = scope == DA2_SCOPE_ROW ? 8 * da2::kCuts * d.BH * d.R : 8 * da2::kCuts * d.BH;
   da2::RankArgs a{};
   a.A = A;
   a.B = (int)d.B;
   a.H = (int)d.H;
   a.R = (int)d.R;
   a.scope = scope;
-  a.T8 = c8;
-  a.T4 = c84 - c8;
+  a.cut[0] = half_up(num16);
+  a.cut[1] = half_up((int64_t)num16 + num8);
+  a.cut[2] = half_up((int64_t)num16 + num8 + num4);
   a.cls = cls;
   a.keys = reinterpret_cast<uint16_t*>(lb + lo[0]);
   a.counts = reinterpret_cast<int32_t*>(lb + lo[1]);
@@ -276,32 +280,35 @@ int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num8, int3
   a.meta = reinterpret_cast<int32_t*>(lb + lo[3]);
   int64_t o = 0;
   a.hist = reinterpret_cast<uint32_t*>(w + o);
-  o += align_up(4 * d.BH * 2 * 2048);
+  o += align_up(4 * d.BH * da2::kCuts * 2048);
   a.thr = reinterpret_cast<uint64_t*>(w + o);
   o += align_up(thr);
   a.prefix = reinterpret_cast<uint64_t*>(w + o);
-  o += align_up(16 * d.BH);
+  o += align_up(8 * da2::kCuts * d.BH);
   a.kleft = reinterpret_cast<int64_t*>(w + o);
-  o += align_up(16 * d.BH);
+  o += align_up(8 * da2::kCuts * d.BH);
   a.cost = reinterpret_cast<int32_t*>(w + o);
   return hip_status(da2::launch_rank(a, static_cast<hipStream_t>(stream)));
 }
 
 int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv, const int32_t* layout,
-                          const da2_problem* p, void* stats, void* ops, void* ws, int64_t ws_bytes, void* stream) {
+                          const da2_problem* p, int32_t with16, void* stats, void* ops, void* ws, int64_t ws_bytes,
+                          void* stream) {
   Dims d;
   int32_t st = derive(p, &d);
   if (st) return st;
   if ((st = check_tensor(qkv, d, false))) return st;
   if (!Q || !K || !V || !layout || !stats || !ops) return DA2_ERR_INVALID_ARG;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V)) return DA2_ERR_INVALID_ARG;
+  if (with16 != 0 && with16 != 1) return DA2_ERR_INVALID_ARG;
   (void)ws;
   if (ws_bytes < 0) return DA2_ERR_WORKSPACE;
   if ((st = check_device())) return st;
-  int64_t off[10];
+  int64_t off[13];
   ops_offsets(d, off);
   char* ob = static_cast<char*>(ops);
   da2::PrepArgs a{};
+  a.with16 = with16;
   a.Q = Q;
   a.K = K;
   a.V = V;
@@ -327,6 +334,9 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
   a.dK = reinterpret_cast<float*>(ob + off[7]);
   a.dV = reinterpret_cast<float*>(ob + off[8]);
   a.g = reinterpret_cast<float*>(ob + off[9]);
+  a.Q16 = reinterpret_cast<_Float16*>(ob + off[10]);
+  a.K16 = reinterpret_cast<_Float16*>(ob + off[11]);
+  a.V16 = reinterpret_cast<_Float16*>(ob + off[12]);
   return hip_status(da2::launch_prep(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -338,7 +348,7 @@ int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout
   if ((st = check_tensor(out, d, true))) return st;
   if (!ops || !lists || !layout || !O) return DA2_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
-  int64_t off[10], lo[4];
+  int64_t off[13], lo[4];
   ops_offsets(d, off);
   lists_offsets(d, lo);
   const char* ob = static_cast<const char*>(ops);
@@ -354,6 +364,9 @@ int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout
   a.dK = reinterpret_cast<const float*>(ob + off[7]);
   a.dV = reinterpret_cast<const float*>(ob + off[8]);
   a.g = reinterpret_cast<const float*>(ob + off[9]);
+  a.Q16 = reinterpret_cast<const _Float16*>(ob + off[10]);
+  a.K16 = reinterpret_cast<const _Float16*>(ob + off[11]);
+  a.V16 = reinterpret_cast<const _Float16*>(ob + off[12]);
   a.keys = reinterpret_cast<const uint16_t*>(lb + lo[0]);
   a.counts = reinterpret_cast<const int32_t*>(lb + lo[1]);
   a.order = reinterpret_cast<const int32_t*>(lb + lo[2]);

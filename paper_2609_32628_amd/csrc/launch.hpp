@@ -20,21 +20,23 @@ struct DraftArgs {
   double *Qbar, *Qmax, *Kbar, *Kmax, *S1, *S2;
 };
 
+constexpr int kCuts = 3;  // rank cut points: T16, T16+T8, T16+T8+T4
+
 struct RankArgs {
   const float* A;
   int B, H, R;
   int scope;
-  int64_t T8, T4;          // quotas per head (head scope) or per row (row scope)
+  int64_t cut[kCuts];      // cumulative quotas per head (head scope) or per row (row scope)
   uint8_t* cls;
   uint16_t* keys;          // lists: [BH*R][R]
-  int32_t* counts;         // [BH*R][2]
+  int32_t* counts;         // [BH*R][4] = (n4, n8, n16, 0)
   int32_t* order;          // [BH*R]
   int32_t* meta;           // [8]
   // workspace
-  uint32_t* hist;          // [BH][2][2048]
-  uint64_t* thr;           // head: [BH][2]; row: [BH*R][2]
-  uint64_t* prefix;        // [BH][2]
-  int64_t* kleft;          // [BH][2]
+  uint32_t* hist;          // [BH][kCuts][2048]
+  uint64_t* thr;           // head: [BH][kCuts]; row: [BH*R][kCuts]
+  uint64_t* prefix;        // [BH][kCuts]
+  int64_t* kleft;          // [BH][kCuts]
   int32_t* cost;           // [BH*R]
 };
 
@@ -52,6 +54,8 @@ struct PrepArgs {
   int8_t *Q8, *K8;
   uint8_t* V8;
   float *dQ, *dK, *dV, *g;
+  _Float16 *Q16, *K16, *V16;  // 16-bit path operands (written when with16)
+  int with16;
 };
 
 struct AttnArgs {
@@ -59,6 +63,7 @@ struct AttnArgs {
   const int8_t *Q8, *K8;
   const uint8_t* V8;
   const float *dQ, *dK, *dV, *g;
+  const _Float16 *Q16, *K16, *V16;
   const uint16_t* keys;
   const int32_t* counts;
   const int32_t* order;

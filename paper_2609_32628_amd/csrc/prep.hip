@@ -13,7 +13,9 @@
 // (16-byte chunks, one per lane of a fragment):
 //   INT8 Q, K with per-block scales, E4M3 V with per-channel scales,
 //   NVFP4 Q, K (16-channel groups) and V (16-slot groups) as the exact fp16
-//   value sigma*e.
+//   value sigma*e,
+//   and, when asked for, the half-precision Q, K, V of the 16-bit path in the
+//   same fragment order as the NVFP4 sections.
 // Scale arithmetic is float32 with one rounding per operation in the documented
 // order (the build uses -ffp-contract=off); division by a scale is a
 // multiplication by its correctly rounded float32 reciprocal. The E2M1 and E4M3
@@ -92,6 +94,14 @@ __global__ __launch_bounds__(256) void prep_vstats_kernel(PrepArgs args) {
 // Row (slot) of MFMA A-operand row r of key tile j: puts the 16-slot group
 // 32j+16g+[0,16) of a query row into lane group g of the 32x32 accumulator.
 __device__ inline int kappa(int j, int r) { return 32 * j + 16 * ((r >> 2) & 1) + 4 * (r >> 3) + (r & 3); }
+
+// Eight values as fp16 (round to nearest even), one 16-byte chunk.
+__device__ inline uint4 half8(const float* x) {
+  f16x8 h;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) h[e] = (_Float16)x[e];
+  return __builtin_bit_cast(uint4, h);
+}
 
 __device__ inline float nvfp4_scale_global(uint32_t amax_bits) {
   const float g = __fdiv_rn(__uint_as_float(amax_bits), 2688.0f);
@@ -209,6 +219,11 @@ __global__ __launch_bounds__(256) void prep_qk_kernel(PrepArgs args) {
     const int64_t c4 = ((int64_t)(jq * NG + c16) * 64 + r) * 8;
     *reinterpret_cast<uint4*>(out4 + c4) = lo;
     *reinterpret_cast<uint4*>(out4 + c4 + 32 * 8) = hi;
+    if (args.with16) {  // 16-bit path: the same chunks as fp16(x)
+      _Float16* out16 = (which == 0 ? args.Q16 : args.K16) + blk * (int64_t)kCap * D;
+      *reinterpret_cast<uint4*>(out16 + c4) = half8(x[k]);
+      *reinterpret_cast<uint4*>(out16 + c4 + 32 * 8) = half8(x[k] + 8);
+    }
   }
 }
 
@@ -285,9 +300,13 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
       // NVFP4 along slots: chunks [t][s = 2 (sg/2) + half][lane][8]
       uint4 lo, hi;
       nvfp4_group16(xc, gV, sixg, lo, hi);
-      _Float16* o4 = args.V4 + blk * (int64_t)kCap * D + ((int64_t)(4 * t + 2 * (sg >> 1)) * 64 + lane) * 8;
-      *reinterpret_cast<uint4*>(o4) = lo;
-      *reinterpret_cast<uint4*>(o4 + 64 * 8) = hi;
+      const int64_t c4 = blk * (int64_t)kCap * D + ((int64_t)(4 * t + 2 * (sg >> 1)) * 64 + lane) * 8;
+      *reinterpret_cast<uint4*>(args.V4 + c4) = lo;
+      *reinterpret_cast<uint4*>(args.V4 + c4 + 64 * 8) = hi;
+      if (args.with16) {  // 16-bit path: the same chunks as fp16(v)
+        *reinterpret_cast<uint4*>(args.V16 + c4) = half8(xc);
+        *reinterpret_cast<uint4*>(args.V16 + c4 + 64 * 8) = half8(xc + 8);
+      }
     }
   }
   if (a == 0) {

@@ -1,12 +1,14 @@
-// Shared ranking kernels (Algorithm 1 without the 16-bit quota; routing appendix).
+// Shared ranking kernels (Algorithm 1; routing appendix).
 //
 // Every region pair gets a unique 54-bit key: the order-preserving image of its
 // float32 score in bits 53..22 and (2^22 - 1 - index) in bits 21..0, so that a
 // larger key means "ranked earlier" under (score descending, index ascending).
-// The pairs of class 8 are exactly those with key >= key of rank T8, and the
-// retained pairs those with key >= key of rank T8+T4 (1-based ranks).
+// With the cumulative quotas cut0 = T16, cut1 = T16 + T8, cut2 = T16 + T8 + T4,
+// the pairs of class 16 are exactly those with key >= key of rank cut0, class
+// 8 those below it with key >= key of rank cut1, and class 4 those below that
+// with key >= key of rank cut2 (1-based ranks; an empty cut matches nothing).
 //
-// Head scope finds both threshold keys with a 5-pass most-significant-digit
+// Head scope finds the three threshold keys with a 5-pass most-significant-digit
 // radix select (11,11,11,11,10 bits) over all R^2 keys of a head: a histogram
 // kernel spread over many workgroups, then a one-workgroup scan per head that
 // fixes the next digit. Row scope sorts each row's R keys in LDS (bitonic).
@@ -31,42 +33,44 @@ __device__ inline uint64_t rank_key(float a, uint32_t idx) {
 
 __global__ void rank_init_kernel(RankArgs args) {
   const int bh = blockIdx.x;
-  for (int i = threadIdx.x; i < 2 * kBins; i += blockDim.x) args.hist[(int64_t)bh * 2 * kBins + i] = 0u;
-  if (threadIdx.x < 2) {
+  for (int i = threadIdx.x; i < kCuts * kBins; i += blockDim.x) args.hist[(int64_t)bh * kCuts * kBins + i] = 0u;
+  if (threadIdx.x < kCuts) {
     const int t = threadIdx.x;
-    args.prefix[bh * 2 + t] = 0ull;
-    args.kleft[bh * 2 + t] = t == 0 ? args.T8 : args.T8 + args.T4;
+    args.prefix[bh * kCuts + t] = 0ull;
+    args.kleft[bh * kCuts + t] = args.cut[t];
   }
 }
 
 __global__ __launch_bounds__(256) void rank_hist_kernel(RankArgs args, int pass) {
-  __shared__ uint32_t lh[2][kBins];
+  __shared__ uint32_t lh[kCuts][kBins];
   const int bh = blockIdx.y;
   const int64_t M = (int64_t)args.R * args.R;
   const int sh = kShift[pass], hi = sh + kWidth[pass];
   const uint64_t mask = (1ull << kWidth[pass]) - 1ull;
-  for (int i = threadIdx.x; i < 2 * kBins; i += 256) (&lh[0][0])[i] = 0u;
-  bool act[2];
-  uint64_t pre[2];
-  for (int t = 0; t < 2; ++t) {
-    act[t] = args.kleft[bh * 2 + t] > 0;
-    pre[t] = args.prefix[bh * 2 + t] >> hi;
+  for (int i = threadIdx.x; i < kCuts * kBins; i += 256) (&lh[0][0])[i] = 0u;
+  bool act[kCuts], any = false;
+  uint64_t pre[kCuts];
+  for (int t = 0; t < kCuts; ++t) {
+    act[t] = args.kleft[bh * kCuts + t] > 0;
+    pre[t] = args.prefix[bh * kCuts + t] >> hi;
+    any = any || act[t];
   }
   __syncthreads();
-  if (act[0] || act[1]) {
+  if (any) {
     const float* A = args.A + (int64_t)bh * M;
     const int64_t e0 = (int64_t)blockIdx.x * kHistChunk;
     const int64_t e1 = e0 + kHistChunk < M ? e0 + kHistChunk : M;
     for (int64_t e = e0 + threadIdx.x; e < e1; e += 256) {
       const uint64_t key = rank_key(A[e], static_cast<uint32_t>(e));
       const uint32_t dig = static_cast<uint32_t>((key >> sh) & mask);
-      if (act[0] && (key >> hi) == pre[0]) atomicAdd(&lh[0][dig], 1u);
-      if (act[1] && (key >> hi) == pre[1]) atomicAdd(&lh[1][dig], 1u);
+#pragma unroll
+      for (int t = 0; t < kCuts; ++t)
+        if (act[t] && (key >> hi) == pre[t]) atomicAdd(&lh[t][dig], 1u);
     }
   }
   __syncthreads();
-  uint32_t* gh = args.hist + (int64_t)bh * 2 * kBins;
-  for (int i = threadIdx.x; i < 2 * kBins; i += 256) {
+  uint32_t* gh = args.hist + (int64_t)bh * kCuts * kBins;
+  for (int i = threadIdx.x; i < kCuts * kBins; i += 256) {
     uint32_t v = (&lh[0][0])[i];
     if (v) atomicAdd(gh + i, v);
   }
@@ -93,9 +97,9 @@ __global__ __launch_bounds__(256) void rank_scan_kernel(RankArgs args, int pass)
   __shared__ uint32_t sh[4];
   const int bh = blockIdx.x;
   const int s = kShift[pass];
-  uint32_t* gh = args.hist + (int64_t)bh * 2 * kBins;
-  for (int t = 0; t < 2; ++t) {
-    const int64_t k = args.kleft[bh * 2 + t];
+  uint32_t* gh = args.hist + (int64_t)bh * kCuts * kBins;
+  for (int t = 0; t < kCuts; ++t) {
+    const int64_t k = args.kleft[bh * kCuts + t];
     if (k <= 0) continue;  // uniform across the block
     // thread i owns bins [2047-8i-7, 2047-8i], visited from the top
     uint32_t c[8], local = 0;
@@ -110,8 +114,8 @@ __global__ __launch_bounds__(256) void rank_scan_kernel(RankArgs args, int pass)
       for (int q = 0; q < 8; ++q) {
         if (k <= (int64_t)run + c[q]) {
           const uint64_t dig = kBins - 1 - 8 * threadIdx.x - q;
-          args.prefix[bh * 2 + t] |= dig << s;
-          args.kleft[bh * 2 + t] = k - run;
+          args.prefix[bh * kCuts + t] |= dig << s;
+          args.kleft[bh * kCuts + t] = k - run;
           break;
         }
         run += c[q];
@@ -119,15 +123,14 @@ __global__ __launch_bounds__(256) void rank_scan_kernel(RankArgs args, int pass)
     }
     __syncthreads();
   }
-  for (int i = threadIdx.x; i < 2 * kBins; i += 256) gh[i] = 0u;
-  if (pass == kPasses - 1 && threadIdx.x < 2) {
+  for (int i = threadIdx.x; i < kCuts * kBins; i += 256) gh[i] = 0u;
+  if (pass == kPasses - 1 && threadIdx.x < kCuts) {
     const int t = threadIdx.x;
-    const int64_t want = t == 0 ? args.T8 : args.T8 + args.T4;
-    args.thr[bh * 2 + t] = want > 0 ? args.prefix[bh * 2 + t] : kNone;
+    args.thr[bh * kCuts + t] = args.cut[t] > 0 ? args.prefix[bh * kCuts + t] : kNone;
   }
 }
 
-// Row scope: sort each row's keys descending in LDS, read the two threshold keys.
+// Row scope: sort each row's keys descending in LDS, read the threshold keys.
 __global__ __launch_bounds__(256) void rank_row_select_kernel(RankArgs args, int P) {
   extern __shared__ uint64_t sk[];
   const int a = blockIdx.x, bh = blockIdx.y, R = args.R;
@@ -150,35 +153,38 @@ __global__ __launch_bounds__(256) void rank_row_select_kernel(RankArgs args, int
       __syncthreads();
     }
   }
-  if (threadIdx.x < 2) {
+  if (threadIdx.x < kCuts) {
     const int t = threadIdx.x;
-    const int64_t want = t == 0 ? args.T8 : args.T8 + args.T4;
-    args.thr[((int64_t)bh * R + a) * 2 + t] = want > 0 ? sk[want - 1] : kNone;
+    const int64_t want = args.cut[t];
+    args.thr[((int64_t)bh * R + a) * kCuts + t] = want > 0 ? sk[want - 1] : kNone;
   }
 }
 
-// Classes, ascending per-row lists (4-bit then 8-bit), counts and row cost.
+// Classes, ascending per-row lists (4-bit, then 8-bit, then 16-bit: the phase
+// order of the attention), counts and row cost.
 __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
   __shared__ uint32_t sh[4];
   const int a = blockIdx.x, bh = blockIdx.y, R = args.R;
   const int64_t row = (int64_t)bh * R + a;
   const float* A = args.A + row * R;
-  const uint64_t* thr = args.scope == DA2_SCOPE_HEAD ? args.thr + (int64_t)bh * 2 : args.thr + row * 2;
-  const uint64_t t8 = thr[0], t84 = thr[1];
+  const uint64_t* thr = args.scope == DA2_SCOPE_HEAD ? args.thr + (int64_t)bh * kCuts : args.thr + row * kCuts;
+  const uint64_t t16 = thr[0], t8 = thr[1], t4 = thr[2];
   uint8_t* cls = args.cls + row * R;
   uint16_t* keys = args.keys + row * R;
   const int lane = threadIdx.x & 63;
-  uint32_t n4 = 0, n8 = 0;
-  for (int want = 4; want <= 8; want += 4) {
-    uint32_t base = want == 4 ? 0u : n4;
+  uint32_t n[3] = {0u, 0u, 0u};  // n4, n8, n16
+  uint32_t base = 0;
+  for (int phase = 0; phase < 3; ++phase) {
+    const int want = 4 << phase;
+    const uint32_t start = base;
     for (int c0 = 0; c0 < R; c0 += 256) {
       const int b = c0 + threadIdx.x;
       int c = 0;
       if (b < R) {
         const uint64_t key = args.scope == DA2_SCOPE_HEAD ? rank_key(A[b], static_cast<uint32_t>(a * R + b))
                                                           : rank_key(A[b], static_cast<uint32_t>(b));
-        c = key >= t8 ? 8 : (key >= t84 ? 4 : 0);
-        if (want == 4) cls[b] = static_cast<uint8_t>(c);
+        c = key >= t16 ? 16 : (key >= t8 ? 8 : (key >= t4 ? 4 : 0));
+        if (phase == 0) cls[b] = static_cast<uint8_t>(c);
       }
       const bool f = c == want;
       const uint64_t m = __ballot(f);
@@ -189,15 +195,14 @@ __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
       if (f) keys[base + wb + in_wave] = static_cast<uint16_t>(b);
       base += tot;
     }
-    if (want == 4)
-      n4 = base;
-    else
-      n8 = base - n4;
+    n[phase] = base - start;
   }
   if (threadIdx.x == 0) {
-    args.counts[row * 2 + 0] = n4;
-    args.counts[row * 2 + 1] = n8;
-    args.cost[row] = 5 * n4 + 4 * n8;
+    args.counts[row * 4 + 0] = n[0];
+    args.counts[row * 4 + 1] = n[1];
+    args.counts[row * 4 + 2] = n[2];
+    args.counts[row * 4 + 3] = 0;
+    args.cost[row] = 5 * n[0] + 4 * n[1] + 5 * n[2];
   }
 }
 
@@ -211,7 +216,7 @@ __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
 constexpr int kOrderBins = 8192;
 __device__ inline int order_key(const RankArgs& args, int64_t i) {
   const int BH = args.B * args.H;
-  const int64_t cmax = 5ll * args.R;
+  const int64_t cmax = 5ll * args.R;  // cost of a row with R 4-bit or 16-bit blocks
   const int groups = 2 * BH;
   const int nbh = groups < kOrderBins ? kOrderBins / groups : 1;  // cost bins per group
   const int bh = (int)(i / args.R), half = (int)(i % args.R) & 1;

@@ -69,6 +69,9 @@ SECTIONS = {
     "Q8": (lambda d: index_q8(d, False), np.int8),
     "K8": (lambda d: index_q8(d, True), np.int8),
     "V8": (index_v8, np.uint8),
+    "Q16": (lambda d: index_q4(d, False), np.float16),   # 16-bit path: the Q4 / K4 / V4 layouts
+    "K16": (lambda d: index_q4(d, True), np.float16),
+    "V16": (index_v4, np.float16),
 }
 
 

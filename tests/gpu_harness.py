@@ -48,7 +48,8 @@ def sections(buf, p):
     out = {}
     specs = [("Q4", np.float16, (R, 64 * d)), ("K4", np.float16, (R, 64 * d)), ("V4", np.float16, (R, 64 * d)),
              ("Q8", np.int8, (R, 64 * d)), ("K8", np.int8, (R, 64 * d)), ("V8", np.uint8, (R, 64 * d)),
-             ("dQ", np.float32, (R,)), ("dK", np.float32, (R,)), ("dV", np.float32, (d,)), ("g", np.float32, (4,))]
+             ("dQ", np.float32, (R,)), ("dK", np.float32, (R,)), ("dV", np.float32, (d,)), ("g", np.float32, (4,)),
+             ("Q16", np.float16, (R, 64 * d)), ("K16", np.float16, (R, 64 * d)), ("V16", np.float16, (R, 64 * d))]
     for i, (name, dt, shape) in enumerate(specs):
         nbytes = BH * int(np.prod(shape)) * np.dtype(dt).itemsize
         out[name] = raw[off[i]:off[i] + nbytes].view(dt).reshape((BH,) + shape)
@@ -60,7 +61,7 @@ def lists_of(buf, p):
     raw = buf.lists.cpu().numpy()
     BH, R = p.B * p.H, buf.sizes["R"]
     keys = raw[lo[0]:lo[0] + 2 * BH * R * R].view(np.uint16).reshape(BH * R, R)
-    counts = raw[lo[1]:lo[1] + 8 * BH * R].view(np.int32).reshape(BH * R, 2)
+    counts = raw[lo[1]:lo[1] + 16 * BH * R].view(np.int32).reshape(BH * R, 4)
     order = raw[lo[2]:lo[2] + 4 * BH * R].view(np.int32)
     return keys, counts, order
 
@@ -70,12 +71,12 @@ def write_lists(buf, p, cls_all):
     lo = api.da2_lists_offsets(p)
     BH, R = cls_all.shape[0], cls_all.shape[1]
     keys = np.zeros((BH * R, R), np.uint16)
-    counts = np.zeros((BH * R, 2), np.int32)
+    counts = np.zeros((BH * R, 4), np.int32)
     for i, row in enumerate(cls_all.reshape(BH * R, R)):
-        l4, l8 = rank.key_lists(row)
-        keys[i, :l4.size] = l4
-        keys[i, l4.size:l4.size + l8.size] = l8
-        counts[i] = (l4.size, l8.size)
+        l4, l8, l16 = rank.key_lists_all(row)
+        seg = np.concatenate([l4, l8, l16])
+        keys[i, :seg.size] = seg
+        counts[i] = (l4.size, l8.size, l16.size, 0)
     raw = buf.lists.cpu().numpy()
     raw[lo[0]:lo[0] + keys.nbytes] = keys.view(np.uint8).reshape(-1)
     raw[lo[1]:lo[1] + counts.nbytes] = counts.view(np.uint8).reshape(-1)
@@ -95,6 +96,8 @@ def expected_sections(enc):
         "V8": to_frag("V8", formats.e4m3_code(enc["v8"])),
         "dQ": enc["dQ"], "dK": enc["dK"], "dV": enc["dV"],
         "g": np.array([enc["gQ"], enc["gK"], enc["gV"], 0], np.float32),
+        "Q16": to_frag("Q16", enc["q16"].astype(np.float64)), "K16": to_frag("K16", enc["k16"].astype(np.float64)),
+        "V16": to_frag("V16", enc["v16"].astype(np.float64)),
     }
 
 
@@ -102,7 +105,7 @@ def write_ops(buf, p, encs):
     """Oracle encodings of every head -> the ops buffer (stage injection)."""
     off = api.da2_ops_offsets(p)
     raw = buf.ops.cpu().numpy()
-    order = ["Q4", "K4", "V4", "Q8", "K8", "V8", "dQ", "dK", "dV", "g"]
+    order = ["Q4", "K4", "V4", "Q8", "K8", "V8", "dQ", "dK", "dV", "g", "Q16", "K16", "V16"]
     for i, name in enumerate(order):
         arr = np.stack([expected_sections(e)[name] for e in encs])
         b = np.ascontiguousarray(arr).view(np.uint8).reshape(-1)
@@ -123,16 +126,19 @@ def compare_outputs(O_gpu, O_ref, label):
     return max_abs, rel
 
 
-def mask_mismatches(cls_gpu, cls_ref, A_ref, T8, T4, scope):
-    """Count class mismatches; every one must be a near-tie at the threshold it crossed."""
+def mask_mismatches(cls_gpu, cls_ref, A_ref, quotas, scope):
+    """Count class mismatches; every one must be a near-tie at a threshold
+    (the score at cumulative rank T16, T16+T8 or T16+T8+T4) it crossed."""
     bad = np.nonzero(cls_gpu != cls_ref)
     if bad[0].size == 0:
         return 0
+    T16, T8, T4 = quotas
+    cuts = (T16, T16 + T8, T16 + T8 + T4)
     R = A_ref.shape[0]
     if scope == "head":
         flat = A_ref.reshape(-1).astype(np.float64)
         order = np.lexsort((np.arange(flat.size), -flat))
-        thetas = [flat[order[k - 1]] for k in (T8, T8 + T4) if k > 0]
+        thetas = [flat[order[k - 1]] for k in cuts if k > 0]
         for a, b in zip(*bad):
             s = float(A_ref[a, b])
             assert min(abs(s - t) / abs(t) for t in thetas) <= NEAR_TIE_REL, (a, b, s, thetas)
@@ -140,7 +146,7 @@ def mask_mismatches(cls_gpu, cls_ref, A_ref, T8, T4, scope):
         for a, b in zip(*bad):
             row = A_ref[a].astype(np.float64)
             order = np.lexsort((np.arange(R), -row))
-            thetas = [row[order[k - 1]] for k in (T8, T8 + T4) if k > 0]
+            thetas = [row[order[k - 1]] for k in cuts if k > 0]
             s = float(A_ref[a, b])
             assert min(abs(s - t) / abs(t) for t in thetas) <= NEAR_TIE_REL, (a, b, s, thetas)
     return bad[0].size

@@ -54,9 +54,9 @@ def test_sizes_mid_layer():
     assert off == sorted(off) and all(o % 256 == 0 for o in off)
     e = 12 * 37632 * 128
     assert off[1] - off[0] >= 2 * e and off[4] - off[3] >= e
-    assert s["ops_bytes"] >= off[9] + 16 * 12
+    assert s["ops_bytes"] >= off[12] + 2 * e and len(off) == 13
     lo = api.da2_lists_offsets(_p(configs.MID))
-    assert lo[1] >= 2 * 12 * 588 * 588 and s["lists_bytes"] >= lo[3] + 32
+    assert lo[1] >= 2 * 12 * 588 * 588 and lo[2] - lo[1] >= 16 * 12 * 588 and s["lists_bytes"] >= lo[3] + 32
     wo = api.da2_ws_draft_offsets(_p(configs.MID))
     assert s["ws_draft_bytes"] >= wo[5] + 8 * 12 * 588 * 588
 
@@ -110,15 +110,17 @@ def test_compute_calls_validate_before_gpu():
     assert L.da2_draft_map(FAKE, FAKE, _desc(sn=64), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
     assert L.da2_draft_map(FAKE, FAKE, d, FAKE, p, 0.2, FAKE, FAKE, FAKE, ws - 1, None) == W
     wr = s["ws_rank_bytes"]
-    for n8, n4, den in [(50, 60, 100), (-1, 10, 100), (10, 10, 0), (10, -5, 100)]:
-        assert L.da2_rank_assign(FAKE, p, n8, n4, den, 0, FAKE, FAKE, FAKE, wr, None) == E
-    assert L.da2_rank_assign(FAKE, p, 10, 30, 100, 3, FAKE, FAKE, FAKE, wr, None) == E
-    assert L.da2_rank_assign(None, p, 10, 30, 100, 0, FAKE, FAKE, FAKE, wr, None) == E
-    assert L.da2_rank_assign(FAKE, p, 10, 30, 100, 0, FAKE, FAKE, FAKE, wr - 1, None) == W
+    for n16, n8, n4, den in [(0, 50, 60, 100), (0, -1, 10, 100), (0, 10, 10, 0), (0, 10, -5, 100), (-1, 10, 10, 100),
+                             (70, 10, 30, 100)]:
+        assert L.da2_rank_assign(FAKE, p, n16, n8, n4, den, 0, FAKE, FAKE, FAKE, wr, None) == E
+    assert L.da2_rank_assign(FAKE, p, 0, 10, 30, 100, 3, FAKE, FAKE, FAKE, wr, None) == E
+    assert L.da2_rank_assign(None, p, 0, 10, 30, 100, 0, FAKE, FAKE, FAKE, wr, None) == E
+    assert L.da2_rank_assign(FAKE, p, 0, 10, 30, 100, 0, FAKE, FAKE, FAKE, wr - 1, None) == W
     big = api.problem(1, 1, 128, 33, 128, 128)           # R^2 >= 2^22 in head scope
-    assert L.da2_rank_assign(FAKE, big, 10, 30, 100, 0, FAKE, FAKE, FAKE, 1 << 40, None) == E
-    assert L.da2_prep_operands(FAKE, None, FAKE, d, FAKE, p, FAKE, FAKE, None, 0, None) == E
-    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(dtype=3), FAKE, p, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_rank_assign(FAKE, big, 0, 10, 30, 100, 0, FAKE, FAKE, FAKE, 1 << 40, None) == E
+    assert L.da2_prep_operands(FAKE, None, FAKE, d, FAKE, p, 0, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(dtype=3), FAKE, p, 0, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, d, FAKE, p, 2, FAKE, FAKE, None, 0, None) == E
     assert L.da2_mixed_attn(FAKE, FAKE, None, p, d, FAKE, None) == E
     assert L.da2_mixed_attn(FAKE, FAKE, FAKE, p, _desc(dtype=9), FAKE, None) == E
 
@@ -134,9 +136,9 @@ def test_inputs_must_allow_16_byte_loads():
     ws = s["ws_draft_bytes"]
     assert L.da2_draft_map(odd, FAKE, _desc(), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
     assert L.da2_draft_map(FAKE, odd, _desc(), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
-    assert L.da2_prep_operands(FAKE, FAKE, odd, _desc(), FAKE, p, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, odd, _desc(), FAKE, p, 0, FAKE, FAKE, None, 0, None) == E
     assert L.da2_draft_map(FAKE, FAKE, _desc(sn=132), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
-    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(sn=130), FAKE, p, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(sn=130), FAKE, p, 0, FAKE, FAKE, None, 0, None) == E
     f32 = _lib.Tensor(12 * 32760 * 128 + 2, 32760 * 128, 128, _lib.DA2_FP32, 0)
     assert L.da2_draft_map(FAKE, FAKE, f32, FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
     # fp32 rows need only 4-element alignment: the stride check passes and the

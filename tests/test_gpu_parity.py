@@ -9,6 +9,8 @@ maxima and statistics bit-exact; the draft map within 1e-6 relative; class
 maps, lists and every encoded byte bit-exact given the same inputs; class
 mismatches end to end only at near-ties (1e-6 relative to the threshold
 score); outputs within max-abs 2e-2 and relative-L2 5e-3 of the oracle."""
+from dataclasses import replace
+
 import numpy as np
 import pytest
 import torch
@@ -43,7 +45,7 @@ def _run_gpu(w, Q, K, V, budgets=None, scope=None, odtype=torch.float32):
     buf = api.alloc(p, scope)
     Qd, Kd, Vd = (to_device(X, w) for X in (Q, K, V))
     O = torch.full(Qd.shape, float("nan"), dtype=odtype, device="cuda")
-    api.attention(Qd, Kd, Vd, buf, w.lam, budgets, O)
+    api.attention(Qd, Kd, Vd, buf, w.lam, budgets, O, num16=w.num16)
     torch.cuda.synchronize()
     return buf, p, O
 
@@ -85,32 +87,33 @@ def _tie_heavy(R, seed):
 
 
 @pytest.mark.parametrize("scope", ["head", "row"])
-@pytest.mark.parametrize("budgets", [(10, 30, 100), (25, 25, 100), (100, 0, 100), (0, 40, 100), (0, 0, 100),
-                                     (5, 95, 100)])
-def test_rank_assign_injected(scope, budgets):
+@pytest.mark.parametrize("budgets16", [(0, 10, 30, 100), (0, 25, 25, 100), (0, 100, 0, 100), (0, 0, 40, 100),
+                                       (0, 0, 0, 100), (0, 5, 95, 100), (15, 10, 30, 100), (100, 0, 0, 100),
+                                       (30, 0, 40, 100)])
+def test_rank_assign_injected(scope, budgets16):
+    num16, budgets = budgets16[0], budgets16[1:]
     w = SMALL
-    log(f"rank_assign parity {scope} {budgets}")
+    log(f"rank_assign parity {scope} {budgets16}")
     p = problem_of(w)
     buf = api.alloc(p, scope)
     R = buf.sizes["R"]
     BH = w.B * w.H
     A = np.stack([_tie_heavy(R, s) for s in range(BH)])
     buf.A.copy_(torch.from_numpy(A.reshape(buf.A.shape)))
-    api.da2_rank_assign(buf.A, p, *budgets, scope, buf.cls, buf.lists, buf.ws_rank)
+    api.da2_rank_assign(buf.A, p, num16, *budgets, scope, buf.cls, buf.lists, buf.ws_rank)
     torch.cuda.synchronize()
     cls = buf.cls.cpu().numpy().reshape(BH, R, R)
     keys, counts, order = lists_of(buf, p)
     assert np.array_equal(np.sort(order), np.arange(BH * R))
     for bh in range(BH):
-        want = orank.rank_head(A[bh], *budgets, scope)
+        want = orank.rank_head(A[bh], *budgets, scope, num16=num16)
         assert np.array_equal(cls[bh], want), bh
         for a in range(R):
-            l4, l8 = orank.key_lists(want[a])
+            l4, l8, l16 = orank.key_lists_all(want[a])
             row = bh * R + a
-            assert tuple(counts[row]) == (l4.size, l8.size)
-            assert np.array_equal(keys[row, :l4.size], l4)
-            assert np.array_equal(keys[row, l4.size:l4.size + l8.size], l8)
-    cost = 5 * counts[:, 0] + 4 * counts[:, 1]
+            assert tuple(counts[row]) == (l4.size, l8.size, l16.size, 0)
+            assert np.array_equal(keys[row, :l4.size + l8.size + l16.size], np.concatenate([l4, l8, l16]))
+    cost = 5 * counts[:, 0] + 4 * counts[:, 1] + 5 * counts[:, 2]
     group = (order // R) * 2 + (order % R) % 2          # (head, row parity) groups in ascending order
     assert np.all(np.diff(group) >= 0)
     same = np.diff(group) == 0
@@ -125,7 +128,7 @@ def test_prep_operands(w):
     buf = api.alloc(p, w.scope)
     Qd, Kd, Vd = (to_device(X, w) for X in (Q, K, V))
     api.da2_draft_map(Qd, Kd, buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
-    api.da2_prep_operands(Qd, Kd, Vd, buf.layout, p, buf.stats, buf.ops, None)
+    api.da2_prep_operands(Qd, Kd, Vd, buf.layout, p, 1, buf.stats, buf.ops, None)
     torch.cuda.synchronize()
     got = sections(buf, p)
     slot2tok, n_a, _ = partition.tile_partition(w.T, w.Hg, w.Wg)
@@ -133,7 +136,7 @@ def test_prep_operands(w):
         b, h = divmod(bh, w.H)
         enc = oenc.encode_head(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
         want = expected_sections(enc)
-        for name in ("Q4", "K4", "V4"):
+        for name in ("Q4", "K4", "V4", "Q16", "K16", "V16"):
             gv, wv = got[name][bh].view(np.uint16), want[name].view(np.uint16)
             assert np.array_equal(gv, wv), (name, bh, int((gv != wv).sum()))
         for name in ("Q8", "K8", "V8"):
@@ -142,13 +145,13 @@ def test_prep_operands(w):
             assert np.array_equal(got[name][bh].view(np.uint32), want[name].view(np.uint32)), (name, bh)
 
 
-def _oracle_encs_cls(w, Q, K, V, budgets, scope):
+def _oracle_encs_cls(w, Q, K, V, budgets, scope, num16=0):
     slot2tok, n_a, _ = partition.tile_partition(w.T, w.Hg, w.Wg)
     encs, clss, outs = [], [], []
     for b in range(w.B):
         for h in range(w.H):
             A32, _ = odraft.draft_head(Q[b, h], K[b, h], slot2tok, n_a, w.lam)
-            cls = orank.rank_head(A32, *budgets, scope)
+            cls = orank.rank_head(A32, *budgets, scope, num16=num16)
             enc = oenc.encode_head(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
             encs.append(enc)
             clss.append(cls)
@@ -156,15 +159,16 @@ def _oracle_encs_cls(w, Q, K, V, budgets, scope):
 
 
 @pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
-@pytest.mark.parametrize("budgets", [None, (100, 0, 100), (20, 20, 100), (5, 45, 100), (0, 40, 100)])
-def test_mixed_attn_injected(w, budgets):
+@pytest.mark.parametrize("budgets16", [None, (0, 100, 0, 100), (0, 20, 20, 100), (0, 5, 45, 100), (0, 0, 40, 100),
+                                       (100, 0, 0, 100), (15, 10, 30, 100), (30, 0, 30, 100)])
+def test_mixed_attn_injected(w, budgets16):
     """Oracle operands and lists in, GPU attention out, oracle attention to compare."""
-    budgets = budgets or w.budgets
-    log(f"mixed_attn stage parity {w.name} {budgets}")
+    num16, budgets = (0, w.budgets) if budgets16 is None else (budgets16[0], budgets16[1:])
+    log(f"mixed_attn stage parity {w.name} {num16} {budgets}")
     Q, K, V = inputs(w)
     p = problem_of(w)
     buf = api.alloc(p, w.scope)
-    encs, clss, (slot2tok, n_a) = _oracle_encs_cls(w, Q, K, V, budgets, w.scope)
+    encs, clss, (slot2tok, n_a) = _oracle_encs_cls(w, Q, K, V, budgets, w.scope, num16)
     write_ops(buf, p, encs)
     write_lists(buf, p, clss)
     O = torch.full((w.B, w.H, w.N, w.d), float("nan"), dtype=torch.float32, device="cuda")
@@ -176,12 +180,14 @@ def test_mixed_attn_injected(w, budgets):
     for bh, (enc, cls) in enumerate(zip(encs, clss)):
         ops = oatt.Operands.quantized(oenc.reconstruct(enc), n_a)
         for a in range(n_a.size):
-            l4, l8 = orank.key_lists(cls[a])
-            ref[bh, slot2tok[a * 64:a * 64 + n_a[a]]] = oatt.attend(ops, a, l4, l8)
-    compare_outputs(Og, ref, f"{w.name} {budgets}")
+            ref[bh, slot2tok[a * 64:a * 64 + n_a[a]]] = oatt.attend(ops, a, *orank.key_lists_all(cls[a]))
+    compare_outputs(Og, ref, f"{w.name} {num16} {budgets}")
 
 
-@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+E2E_CASES = CASES + [replace(SMALL, name="small-16bit-15/10/30", num16=15)]
+
+
+@pytest.mark.parametrize("w", E2E_CASES, ids=lambda w: w.name)
 def test_end_to_end(w):
     log(f"end-to-end parity {w.name}")
     Q, K, V = inputs(w)
@@ -192,9 +198,11 @@ def test_end_to_end(w):
     cls_g = buf.cls.cpu().numpy().reshape(-1, R, R)
     Og = O.cpu().numpy().reshape(-1, w.N, w.d)
     M = R * R if w.scope == "head" else R
-    T8, T4 = orank.quotas(*w.budgets, M)
+    T16, T8, T4 = orank.quotas3(w.num16, *w.budgets, M)
     for bh, o in enumerate(outs):
-        n_bad = mask_mismatches(cls_g[bh], o["cls"], o["A32"], T8, T4, w.scope)
+        assert [(cls_g[bh] == c).sum() for c in (16, 8, 4)] == ([T16, T8, T4] if w.scope == "head"
+                                                                 else [T16 * R, T8 * R, T4 * R])
+        n_bad = mask_mismatches(cls_g[bh], o["cls"], o["A32"], (T16, T8, T4), w.scope)
         ref = o["O"].copy()
         if n_bad:   # rows whose masks differ at a near-tie are compared only through the mask check
             for a in np.nonzero((cls_g[bh] != o["cls"]).any(axis=1))[0]:
@@ -219,7 +227,7 @@ def test_mid_layer_sampled_rows():
     for h in (0, 7):
         layout, outs = pipeline.run(w, Q[:, h:h + 1], K[:, h:h + 1], V[:, h:h + 1], rows=rows)
         o = outs[0]
-        n_bad = mask_mismatches(cls_g[0, h], o["cls"], o["A32"], T8, T4, "head")
+        n_bad = mask_mismatches(cls_g[0, h], o["cls"], o["A32"], (0, T8, T4), "head")
         log(f"  head {h}: near-tie mask mismatches {n_bad}")
         ref = o["O"].copy()
         slot2tok, n_a, _ = layout
