@@ -27,6 +27,8 @@ import re
 import sys
 import time
 
+from dataclasses import replace
+
 import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -71,6 +73,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mid-21x30x52-h12-d128")
+    ap.add_argument("--num16", type=int, default=None,
+                    help="num16/den of the region pairs on the 16-bit path (the hot path uses 0)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 512 MiB device copy (HBM counter calibration)")
@@ -90,13 +94,12 @@ def cpu_baseline(w, Q, K, V):
     q, k, v = Q[0, 0], K[0, 0], V[0, 0]
     t0 = time.perf_counter()
     A32, _ = draft.draft_head(q, k, slot2tok, n_a, w.lam)
-    cls = rank.rank_head(A32, *w.budgets, w.scope)
+    cls = rank.rank_head(A32, *w.budgets, w.scope, num16=w.num16)
     enc = encode.encode_head(q, k, v, slot2tok, n_a)
     ops = attention.Operands.quantized(encode.reconstruct(enc), n_a)
     t1 = time.perf_counter()
     for a in rows:
-        l4, l8 = rank.key_lists(cls[a])
-        attention.attend(ops, a, l4, l8)
+        attention.attend(ops, a, *rank.key_lists_all(cls[a]))
     t2 = time.perf_counter()
     per_head = (t1 - t0) + (t2 - t1) / len(rows) * R
     t_job = per_head * w.H * w.B
@@ -120,6 +123,8 @@ def main():
     from synth import configs, gen
 
     w = configs.BY_NAME[args.workload]
+    if args.num16 is not None:
+        w = replace(w, num16=args.num16)
     Q, K, V = gen.generate(w)
     dev = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (Q, K, V)]
     p = api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg)
@@ -171,11 +176,12 @@ def main():
     counts = buf.cls.view(w.B * w.H, -1)
     n8 = int((counts == 8).sum().item())
     n4 = int((counts == 4).sum().item())
+    n16 = int((counts == 16).sum().item())
     tile_flops = 4.0 * 64 * 64 * w.d
-    F8, F4 = n8 * tile_flops, n4 * tile_flops
+    F8, F4, F16 = n8 * tile_flops, n4 * tile_flops, n16 * tile_flops
     t_attn = stage_ms["mixed_attn"] * 1e-3
-    achieved = (F8 + F4) / t_attn
-    peak_eff = (F8 + F4) / (F8 / PEAK_8BIT + F4 / PEAK_FP16)
+    achieved = (F8 + F4 + F16) / t_attn
+    peak_eff = (F8 + F4 + F16) / (F8 / PEAK_8BIT + (F4 + F16) / PEAK_FP16)
     dense_flops = 4.0 * w.B * w.H * w.N ** 2 * w.d
     # bytes each preparation call must move (bf16 inputs)
     sizes = buf.sizes
@@ -200,18 +206,18 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "heads": w.H, "tokens": w.N, "d": w.d,
                    "grid": [w.T, w.Hg, w.Wg], "budgets_8_4_skip": [w.budgets[0], w.budgets[1],
-                                                                   w.budgets[2] - w.budgets[0] - w.budgets[1]],
-                   "scope": w.scope, "lambda": w.lam, "parallelism": "single GPU"},
+                                                                   w.budgets[2] - w.budgets[0] - w.budgets[1] - w.num16],
+                   "scope": w.scope, "lambda": w.lam, "num16": w.num16, "parallelism": "single GPU"},
         "stage_ms": stage_ms,
         "mixed_attn_ms": stage_ms["mixed_attn"],
         "mixed_attn_dense_equiv_tflops": dense_flops / t_attn / 1e12,
-        "tiles": {"8bit": n8, "4bit": n4},
+        "tiles": {"8bit": n8, "4bit": n4, "16bit": n16},
         "roofline": {"bound": "mfma", "kernel": "mixed_attn_kernel", "achieved": achieved / 1e12,
                      "peak": peak_eff / 1e12, "unit": "TFLOP/s", "frac": achieved / peak_eff,
                      "traffic": recorded_traffic(w.name),
                      "peak_note": "budget-weighted: 8-bit tiles at 5.0 PF (int8/fp8), 4-bit tiles at 2.5 PF "
-                                  "(fp16 MFMA on exact NVFP4 reconstructions)",
-                     "frac_vs_fp4_peak": achieved * (F8 / PEAK_8BIT + F4 / 10.0e15) / (F8 + F4)},
+                                  "(fp16 MFMA on exact NVFP4 reconstructions), 16-bit tiles at 2.5 PF",
+                     "frac_vs_fp4_peak": achieved * (F8 / PEAK_8BIT + F4 / 10.0e15 + F16 / PEAK_FP16) / (F8 + F4 + F16)},
         "hbm": hbm,
     }
     if not args.no_cpu_baseline:
