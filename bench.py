@@ -73,6 +73,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mid-21x30x52-h12-d128")
+    ap.add_argument("--partition", choices=("tiles8", "ragged"), default=None,
+                    help="region partition (the configured workloads use 8x8 tiles)")
     ap.add_argument("--num16", type=int, default=None,
                     help="num16/den of the region pairs on the 16-bit path (the hot path uses 0)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -87,7 +89,7 @@ def cpu_baseline(w, Q, K, V):
     from threadpoolctl import threadpool_info
 
     from oracle import attention, draft, encode, partition, rank
-    slot2tok, n_a, _ = partition.tile_partition(w.T, w.Hg, w.Wg)
+    slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
     R = n_a.size
     rng = np.random.default_rng(0)
     rows = sorted(rng.choice(R, min(R, 288), replace=False))
@@ -125,9 +127,11 @@ def main():
     w = configs.BY_NAME[args.workload]
     if args.num16 is not None:
         w = replace(w, num16=args.num16)
+    if args.partition is not None:
+        w = replace(w, partition=args.partition)
     Q, K, V = gen.generate(w)
     dev = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (Q, K, V)]
-    p = api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg)
+    p = api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg, w.partition)
     buf = api.alloc(p, w.scope)
     O = torch.empty(dev[0].shape, dtype=torch.bfloat16, device="cuda")
     stream = torch.cuda.current_stream()
@@ -207,7 +211,8 @@ def main():
         "config": {"workload": w.name, "B": w.B, "heads": w.H, "tokens": w.N, "d": w.d,
                    "grid": [w.T, w.Hg, w.Wg], "budgets_8_4_skip": [w.budgets[0], w.budgets[1],
                                                                    w.budgets[2] - w.budgets[0] - w.budgets[1] - w.num16],
-                   "scope": w.scope, "lambda": w.lam, "num16": w.num16, "parallelism": "single GPU"},
+                   "scope": w.scope, "lambda": w.lam, "num16": w.num16, "partition": w.partition,
+                   "parallelism": "single GPU"},
         "stage_ms": stage_ms,
         "mixed_attn_ms": stage_ms["mixed_attn"],
         "mixed_attn_dense_equiv_tflops": dense_flops / t_attn / 1e12,

@@ -13,11 +13,23 @@
  *
  * Conventions for every call
  * --------------------------
- * - Regions are 8x8 spatial tiles of each frame (capacity C = 64 tokens).
- *   Tokens are numbered frame-major raster: n = t*Hg*Wg + y*Wg + x. Block
- *   a = (t*nI + i)*nJ + j with nI = ceil(Hg/8), nJ = ceil(Wg/8); R = T*nI*nJ
- *   blocks, Npad = 64*R slots. The slots of a block hold its valid tokens in
- *   row-major order, then padding.
+ * - Tokens are numbered frame-major raster: n = t*Hg*Wg + y*Wg + x. Each
+ *   frame is split into R_f regions of at most C = 64 tokens (p->partition):
+ *   DA2_PART_TILES8: 8x8 spatial tiles, block a = (t*nI + i)*nJ + j with
+ *     nI = ceil(Hg/8), nJ = ceil(Wg/8), R_f = nI*nJ;
+ *   DA2_PART_RAGGED (fused-reordering paragraph, ragged-padding and
+ *     region-perimeter equations): R_f = ceil(Hg*Wg/64) connected regions
+ *     with less than one block of padding per frame. Candidates split the
+ *     frame into nb bands of balanced height (larger first), along rows or
+ *     along columns; each band is walked in a snake order (down one column
+ *     and up the next; along one row and back for column bands) and cut into
+ *     ceil(band/64) consecutive runs of balanced size (larger first). Valid
+ *     candidates have R_f runs; the smallest total perimeter (fewest
+ *     neighbour pairs split between regions) wins, then row bands, then
+ *     fewer bands. Regions are numbered band by band, run by run, and block
+ *     a = t*R_f + region.
+ *   R = T*R_f blocks, Npad = 64*R slots. The slots of a block hold its valid
+ *   tokens in row-major order, then padding.
  * - Every device buffer is allocated and owned by the caller; sizes come from
  *   da2_sizes(). The library never allocates or frees device memory, never
  *   synchronizes the host and keeps no mutable global state. Buffers that a
@@ -52,10 +64,17 @@ typedef enum {
 typedef enum { DA2_BF16 = 0, DA2_FP32 = 1 } da2_dtype;
 typedef enum { DA2_SCOPE_HEAD = 0, DA2_SCOPE_ROW = 1 } da2_scope;
 
+/* Region partitions of each frame (capacity C = 64 slots per block). */
+typedef enum {
+  DA2_PART_TILES8 = 0, /* 8x8 spatial tiles: R_f = ceil(Hg/8)*ceil(Wg/8) blocks per frame */
+  DA2_PART_RAGGED = 1  /* ragged minimum-perimeter regions: R_f = ceil(Hg*Wg/64) */
+} da2_partition;
+
 /* Problem shape: batch B, heads H, head dim d, latent grid T x Hg x Wg
- * (N = T*Hg*Wg tokens). */
+ * (N = T*Hg*Wg tokens), region partition (da2_partition). */
 typedef struct {
   int32_t B, H, d, T, Hg, Wg;
+  int32_t partition;
 } da2_problem;
 
 /* A [B, H, N, d] tensor with d contiguous; strides are in elements. Input
@@ -84,7 +103,8 @@ typedef struct {
 const char* da2_status_string(int32_t status);
 
 /* Host only. Fills *out for problem p; ranking scope affects ws_rank_bytes.
- * Errors: INVALID_ARG for non-positive dims, d not in {64,128}, or sizes that
+ * Errors: INVALID_ARG for non-positive dims, d not in {64,128}, an unknown
+ * partition, or sizes that
  * overflow the index types or launch grids (R > 65535 blocks, B*H > 32767,
  * B*H*R > 2^31-1). */
 int32_t da2_sizes(const da2_problem* p, int32_t scope, da2_sizes_t* out);

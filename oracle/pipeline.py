@@ -35,7 +35,7 @@ def run_head(Q, K, V, layout, lam, budgets, scope, rows=None, mode="quant", num1
 
 def run(w, Q, K, V, heads=None, rows=None, mode="quant"):
     """Whole workload ``w`` (synth.configs.Workload). Q, K, V: [B, H, N, d]."""
-    layout = partition.tile_partition(w.T, w.Hg, w.Wg)
+    layout = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
     out = []
     for b in range(Q.shape[0]):
         for h in (range(Q.shape[1]) if heads is None else heads):

@@ -12,6 +12,7 @@ LIB_PATH = os.path.join(HERE, "libda2.so")
 DA2_OK, DA2_ERR_INVALID_ARG, DA2_ERR_UNSUPPORTED, DA2_ERR_WORKSPACE, DA2_ERR_HIP = 0, -1, -2, -3, -4
 DA2_BF16, DA2_FP32 = 0, 1
 DA2_SCOPE_HEAD, DA2_SCOPE_ROW = 0, 1
+DA2_PART_TILES8, DA2_PART_RAGGED = 0, 1
 
 # Every symbol include/da2.h declares.
 EXPORTS = ("da2_status_string", "da2_sizes", "da2_layout_build", "da2_draft_map", "da2_ws_draft_offsets",
@@ -20,7 +21,8 @@ EXPORTS = ("da2_status_string", "da2_sizes", "da2_layout_build", "da2_draft_map"
 
 class Problem(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
-                ("T", ctypes.c_int32), ("Hg", ctypes.c_int32), ("Wg", ctypes.c_int32)]
+                ("T", ctypes.c_int32), ("Hg", ctypes.c_int32), ("Wg", ctypes.c_int32),
+                ("partition", ctypes.c_int32)]
 
 
 class Tensor(ctypes.Structure):

@@ -12,13 +12,15 @@ import numpy as np
 import torch
 
 from . import _lib
-from ._lib import DA2_BF16, DA2_FP32, DA2_SCOPE_HEAD, DA2_SCOPE_ROW, Problem, Tensor, check, lib
+from ._lib import (DA2_BF16, DA2_FP32, DA2_PART_RAGGED, DA2_PART_TILES8, DA2_SCOPE_HEAD, DA2_SCOPE_ROW, Problem,
+                   Tensor, check, lib)
 
 SCOPES = {"head": DA2_SCOPE_HEAD, "row": DA2_SCOPE_ROW}
+PARTITIONS = {"tiles8": DA2_PART_TILES8, "ragged": DA2_PART_RAGGED}
 
 
-def problem(B, H, d, T, Hg, Wg):
-    return Problem(B, H, d, T, Hg, Wg)
+def problem(B, H, d, T, Hg, Wg, partition="tiles8"):
+    return Problem(B, H, d, T, Hg, Wg, PARTITIONS[partition])
 
 
 def _tensor_desc(x):

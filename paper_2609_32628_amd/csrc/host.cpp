@@ -3,9 +3,11 @@
 // GPU, so every error path can be exercised on a machine without one.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstring>
+#include <vector>
 
 #include "../../include/da2.h"
 #include "launch.hpp"
@@ -17,12 +19,15 @@ inline int64_t align_up(int64_t x) { return (x + kAlign - 1) / kAlign * kAlign; 
 
 struct Dims {
   int64_t B, H, d, T, Hg, Wg, N, R, Npad, BH;
+  int64_t Rf;  // blocks per frame
+  int32_t partition;
 };
 
 int32_t derive(const da2_problem* p, Dims* o) {
   if (!p) return DA2_ERR_INVALID_ARG;
   if (p->B <= 0 || p->H <= 0 || p->T <= 0 || p->Hg <= 0 || p->Wg <= 0 || p->d <= 0) return DA2_ERR_INVALID_ARG;
   if (p->d != 64 && p->d != 128) return DA2_ERR_INVALID_ARG;
+  if (p->partition != DA2_PART_TILES8 && p->partition != DA2_PART_RAGGED) return DA2_ERR_INVALID_ARG;
   Dims d{};
   d.B = p->B;
   d.H = p->H;
@@ -31,7 +36,9 @@ int32_t derive(const da2_problem* p, Dims* o) {
   d.Hg = p->Hg;
   d.Wg = p->Wg;
   d.N = d.T * d.Hg * d.Wg;
-  d.R = d.T * ((d.Hg + 7) / 8) * ((d.Wg + 7) / 8);
+  d.partition = p->partition;
+  d.Rf = d.partition == DA2_PART_TILES8 ? ((d.Hg + 7) / 8) * ((d.Wg + 7) / 8) : (d.Hg * d.Wg + 63) / 64;
+  d.R = d.T * d.Rf;
   d.Npad = 64 * d.R;
   d.BH = d.B * d.H;
   // launch grids put R and 2*B*H in 16-bit grid dimensions
@@ -119,6 +126,54 @@ int32_t check_device() {
 
 int32_t hip_status(hipError_t e) { return e == hipSuccess ? DA2_OK : DA2_ERR_HIP; }
 
+// Ragged partition of one H x W frame (the candidate family documented in
+// da2.h): the label of every cell, row-major.
+std::vector<int32_t> ragged_frame_labels(int64_t H, int64_t W) {
+  constexpr int64_t C = 64;
+  const int64_t Rf = (H * W + C - 1) / C;
+  std::vector<int32_t> best, cand(H * W);
+  int64_t best_key[3] = {0, 0, 0};
+  for (int orient = 0; orient < 2; ++orient) {
+    // bands split the first axis of the (h, w) view; orient 1 is the transposed frame
+    const int64_t h = orient == 0 ? H : W, w = orient == 0 ? W : H;
+    for (int64_t nb = 1; nb <= h; ++nb) {
+      int64_t runs = 0;
+      for (int64_t i = 0; i < nb; ++i) runs += ((h / nb + (i < h % nb ? 1 : 0)) * w + C - 1) / C;
+      if (runs != Rf) continue;
+      int64_t y0 = 0, label = 0;
+      for (int64_t i = 0; i < nb; ++i) {
+        const int64_t hb = h / nb + (i < h % nb ? 1 : 0), n = hb * w, r = (n + C - 1) / C;
+        int64_t k = 0, used = 0, size = n / r + (0 < n % r ? 1 : 0);
+        for (int64_t c = 0; c < w; ++c)
+          for (int64_t q = 0; q < hb; ++q) {
+            const int64_t yy = y0 + (c % 2 == 0 ? q : hb - 1 - q);  // snake down / up the column
+            const int64_t idx = orient == 0 ? yy * W + c : c * W + yy;
+            cand[idx] = (int32_t)(label + k);
+            if (++used == size && k + 1 < r) {
+              ++k;
+              used = 0;
+              size = n / r + (k < n % r ? 1 : 0);
+            }
+          }
+        y0 += hb;
+        label += r;
+      }
+      int64_t cut = 0;
+      for (int64_t y = 0; y < H; ++y)
+        for (int64_t x = 0; x < W; ++x) {
+          if (x + 1 < W && cand[y * W + x] != cand[y * W + x + 1]) ++cut;
+          if (y + 1 < H && cand[y * W + x] != cand[(y + 1) * W + x]) ++cut;
+        }
+      const int64_t key[3] = {cut, orient, nb};
+      if (best.empty() || std::lexicographical_compare(key, key + 3, best_key, best_key + 3)) {
+        best = cand;
+        std::copy(key, key + 3, best_key);
+      }
+    }
+  }
+  return best;
+}
+
 }  // namespace
 
 extern "C" {
@@ -175,25 +230,29 @@ int32_t da2_layout_build(const da2_problem* p, int32_t* L, int64_t n_ints) {
   int32_t st = derive(p, &d);
   if (st) return st;
   if (!L || n_ints < d.R + d.Npad + d.N) return DA2_ERR_INVALID_ARG;
-  const int64_t nI = (d.Hg + 7) / 8, nJ = (d.Wg + 7) / 8;
+  // region label of every cell of a frame
+  std::vector<int32_t> lab;
+  if (d.partition == DA2_PART_TILES8) {
+    const int64_t nJ = (d.Wg + 7) / 8;
+    lab.resize(d.Hg * d.Wg);
+    for (int64_t y = 0; y < d.Hg; ++y)
+      for (int64_t x = 0; x < d.Wg; ++x) lab[y * d.Wg + x] = (int32_t)((y / 8) * nJ + x / 8);
+  } else {
+    lab = ragged_frame_labels(d.Hg, d.Wg);
+  }
   int32_t* n_a = L;
   int32_t* s2t = L + d.R;
   int32_t* t2s = L + d.R + d.Npad;
   for (int64_t i = 0; i < d.Npad; ++i) s2t[i] = -1;
+  for (int64_t a = 0; a < d.R; ++a) n_a[a] = 0;
   for (int64_t t = 0; t < d.T; ++t)
-    for (int64_t i = 0; i < nI; ++i)
-      for (int64_t j = 0; j < nJ; ++j) {
-        const int64_t a = (t * nI + i) * nJ + j;
-        const int64_t y1 = i * 8 + 8 < d.Hg ? i * 8 + 8 : d.Hg, x1 = j * 8 + 8 < d.Wg ? j * 8 + 8 : d.Wg;
-        int32_t s = 0;
-        for (int64_t y = i * 8; y < y1; ++y)
-          for (int64_t x = j * 8; x < x1; ++x) {
-            const int64_t tok = t * d.Hg * d.Wg + y * d.Wg + x;
-            s2t[a * 64 + s] = (int32_t)tok;
-            t2s[tok] = (int32_t)(a * 64 + s);
-            ++s;
-          }
-        n_a[a] = s;
+    for (int64_t y = 0; y < d.Hg; ++y)  // row-major, so each block's slots come out row-major
+      for (int64_t x = 0; x < d.Wg; ++x) {
+        const int64_t a = t * d.Rf + lab[y * d.Wg + x];
+        const int64_t tok = t * d.Hg * d.Wg + y * d.Wg + x;
+        const int64_t slot = a * 64 + n_a[a]++;
+        s2t[slot] = (int32_t)tok;
+        t2s[tok] = (int32_t)slot;
       }
   return DA2_OK;
 }

@@ -32,6 +32,7 @@ class Workload:
     lam: float = 0.2                # pooling weight lambda of the draft map
     seed: int = 0
     num16: int = 0                  # num16/den of the pairs go to the 16-bit path
+    partition: str = "tiles8"       # "tiles8" (8x8 tiles) or "ragged" (minimum-perimeter regions)
 
     @property
     def N(self) -> int:

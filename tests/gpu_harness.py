@@ -27,7 +27,7 @@ def log(*a):
 
 
 def problem_of(w):
-    return api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg)
+    return api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg, w.partition)
 
 
 def inputs(w, heads=None):

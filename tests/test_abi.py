@@ -72,12 +72,30 @@ def test_layout_matches_tile_definition(T, Hg, Wg):
     assert np.array_equal(L[R + 64 * R:], tok2slot)
 
 
+@pytest.mark.parametrize("T,Hg,Wg", [(2, 16, 16), (2, 13, 11), (3, 7, 17), (21, 30, 52), (1, 45, 80), (1, 2, 100),
+                                     (1, 100, 2), (2, 1, 1), (1, 33, 7)])
+def test_ragged_layout_matches_oracle_partition(T, Hg, Wg):
+    """The library's ragged layout (host C++) and the oracle's ragged partition
+    (independent Python) give the same blocks, slots and inverse map."""
+    p = api.problem(1, 1, 64, T, Hg, Wg, "ragged")
+    L = api.da2_layout_build(p)
+    slot2tok, n_a, tok2slot = partition.ragged_partition(T, Hg, Wg)
+    R = n_a.size
+    assert api.da2_sizes(p)["R"] == R == T * (-(-Hg * Wg // 64))
+    assert np.array_equal(L[:R], n_a)
+    assert np.array_equal(L[R:R + 64 * R], slot2tok)
+    assert np.array_equal(L[R + 64 * R:], tok2slot)
+
+
 def test_invalid_problems():
     s = _lib.Sizes()
     L = _lib.lib()
     for bad in [(0, 1, 64, 1, 8, 8), (1, 1, 96, 1, 8, 8), (1, 1, 128, 1, 0, 8), (1, 1, 128, -1, 8, 8)]:
         assert L.da2_sizes(ctypes.byref(api.problem(*bad)), 0, ctypes.byref(s)) == _lib.DA2_ERR_INVALID_ARG
     assert L.da2_sizes(ctypes.byref(api.problem(1, 1, 64, 1, 8, 8)), 5, ctypes.byref(s)) == _lib.DA2_ERR_INVALID_ARG
+    odd = api.problem(1, 1, 64, 1, 8, 8)
+    odd.partition = 2
+    assert L.da2_sizes(ctypes.byref(odd), 0, ctypes.byref(s)) == _lib.DA2_ERR_INVALID_ARG
     assert L.da2_sizes(None, 0, ctypes.byref(s)) == _lib.DA2_ERR_INVALID_ARG
     # more than 65535 blocks
     assert L.da2_sizes(ctypes.byref(api.problem(1, 1, 64, 2000, 80, 80)), 0, ctypes.byref(s)) == _lib.DA2_ERR_INVALID_ARG

@@ -24,6 +24,7 @@ from synth import configs
 pytestmark = pytest.mark.gpu
 
 CASES = [configs.TINY, SMALL]
+SMALL_RAGGED = replace(SMALL, name="small-ragged-3x13x21", partition="ragged")
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -50,7 +51,7 @@ def _run_gpu(w, Q, K, V, budgets=None, scope=None, odtype=torch.float32):
     return buf, p, O
 
 
-@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED], ids=lambda w: w.name)
 def test_draft_map(w):
     log(f"draft_map parity {w.name}")
     Q, K, V = inputs(w)
@@ -59,7 +60,7 @@ def test_draft_map(w):
     Qd, Kd = to_device(Q, w), to_device(K, w)
     api.da2_draft_map(Qd, Kd, buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
     torch.cuda.synchronize()
-    slot2tok, n_a, _ = partition.tile_partition(w.T, w.Hg, w.Wg)
+    slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
     R, d = n_a.size, w.d
     A = buf.A.cpu().numpy().reshape(-1, R, R)
     ws = buf.ws_draft.cpu().numpy()
@@ -120,7 +121,7 @@ def test_rank_assign_injected(scope, budgets16):
     assert np.all(np.diff(cost[order])[same] <= 5 * R * 2 * BH // 8192 + 5)   # longest first within a group
 
 
-@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED], ids=lambda w: w.name)
 def test_prep_operands(w):
     log(f"prep_operands parity {w.name}")
     Q, K, V = inputs(w)
@@ -131,7 +132,7 @@ def test_prep_operands(w):
     api.da2_prep_operands(Qd, Kd, Vd, buf.layout, p, 1, buf.stats, buf.ops, None)
     torch.cuda.synchronize()
     got = sections(buf, p)
-    slot2tok, n_a, _ = partition.tile_partition(w.T, w.Hg, w.Wg)
+    slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
     for bh in range(w.B * w.H):
         b, h = divmod(bh, w.H)
         enc = oenc.encode_head(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
@@ -146,7 +147,7 @@ def test_prep_operands(w):
 
 
 def _oracle_encs_cls(w, Q, K, V, budgets, scope, num16=0):
-    slot2tok, n_a, _ = partition.tile_partition(w.T, w.Hg, w.Wg)
+    slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
     encs, clss, outs = [], [], []
     for b in range(w.B):
         for h in range(w.H):
@@ -184,7 +185,8 @@ def test_mixed_attn_injected(w, budgets16):
     compare_outputs(Og, ref, f"{w.name} {num16} {budgets}")
 
 
-E2E_CASES = CASES + [replace(SMALL, name="small-16bit-15/10/30", num16=15)]
+E2E_CASES = CASES + [replace(SMALL, name="small-16bit-15/10/30", num16=15), SMALL_RAGGED,
+                     replace(SMALL_RAGGED, name="small-ragged-16bit", num16=20, scope="row")]
 
 
 @pytest.mark.parametrize("w", E2E_CASES, ids=lambda w: w.name)
@@ -235,6 +237,28 @@ def test_mid_layer_sampled_rows():
             ref[slot2tok[a * 64:a * 64 + n_a[a]]] = np.nan
         compare_outputs(Og[0, h], ref, f"mid head {h}")
         assert (cls_g[0, h] == 8).sum() == T8 and (cls_g[0, h] == 4).sum() == T4
+
+
+def test_mid_layer_ragged_sampled_rows():
+    """The mid layer on the ragged partition (25 regions per frame, R = 525)."""
+    w = replace(configs.MID, partition="ragged")
+    log("end-to-end parity mid layer, ragged partition, sampled rows")
+    Q, K, V = inputs(w, heads=[3])
+    w1 = replace(w, H=1)
+    buf, p, O = _run_gpu(w1, Q, K, V)
+    R = buf.sizes["R"]
+    assert R == 21 * 25
+    rows = sorted(np.random.default_rng(1).choice(R, 16, replace=False))
+    layout, outs = pipeline.run(w1, Q, K, V, rows=rows)
+    o = outs[0]
+    T8, T4 = orank.quotas(*w.budgets, R * R)
+    cls_g = buf.cls.cpu().numpy().reshape(R, R)
+    n_bad = mask_mismatches(cls_g, o["cls"], o["A32"], (0, T8, T4), "head")
+    ref = o["O"].copy()
+    slot2tok, n_a, _ = layout
+    for a in np.nonzero((cls_g != o["cls"]).any(axis=1))[0]:
+        ref[slot2tok[a * 64:a * 64 + n_a[a]]] = np.nan
+    compare_outputs(O.cpu().numpy()[0, 0], ref, f"mid ragged (head 3 inputs), near-tie mismatches {n_bad}")
 
 
 def test_bf16_output_and_determinism():
