@@ -61,6 +61,20 @@ def quant_weights_fp8(Pt):
     return ETA * e4m3(AMP * Pt)
 
 
+MX_GROUP = 32
+
+
+def quant_weights_mx(Pt):
+    """MXFP4 weights for Pt [..., 64]: 32-slot blocks, X = 2^(floor(log2 max) - 2)
+    (clamped to [2^-127, 2^127]), w = X E2M1(Pt / X); a zero block stays zero."""
+    g = np.asarray(Pt, np.float64).reshape(Pt.shape[:-1] + (CAP // MX_GROUP, MX_GROUP))
+    amax = g.max(axis=-1)
+    _, e = np.frexp(np.where(amax > 0, amax, 1.0))
+    k = np.where(amax > 0, np.clip((e - 1) - 2, -127, 127), -127)
+    X = np.ldexp(1.0, k)[..., None]
+    return (X * e2m1(g / X)).reshape(Pt.shape)
+
+
 def quant_weights_fp16(Pt):
     """16-bit path weights: Pt cast to IEEE half precision (round to nearest even)."""
     return np.asarray(Pt, np.float64).astype(np.float16).astype(np.float64)
@@ -80,7 +94,13 @@ class Operands:
         self.phases = phases
 
     @classmethod
-    def quantized(cls, rec, n_a):
+    def quantized(cls, rec, n_a, rec_mx=None):
+        """Quantized operands; with ``rec_mx`` (reconstruct_mx) the 4-bit phase
+        runs on MXFP4 operands and weights instead of NVFP4."""
+        if rec_mx is not None:
+            return cls(n_a, {4: (rec_mx["Qh4"], rec_mx["Kh4"], rec_mx["Vh4"], quant_weights_mx),
+                             8: (rec["Qh8"], rec["Kh8"], rec["Vh8"], quant_weights_fp8),
+                             16: (rec["Qh16"], rec["Kh16"], rec["Vh16"], quant_weights_fp16)})
         return cls(n_a, {4: (rec["Qh4"], rec["Kh4"], rec["Vh4"], quant_weights_fp4),
                          8: (rec["Qh8"], rec["Kh8"], rec["Vh8"], quant_weights_fp8),
                          16: (rec["Qh16"], rec["Kh16"], rec["Vh16"], quant_weights_fp16)})
@@ -130,7 +150,7 @@ def attend(ops, a, list4, list8, list16=(), return_parts=False):
     return O
 
 
-def attend_sequential(ops, a, list4, list8, dV, gV, list16=()):
+def attend_sequential(ops, a, list4, list8, dV, gV, list16=(), mx=False):
     """The online recurrence block by block, with the phase unit changes.
 
     Phase 4 accumulates U in units of g_V/2688 (its matrix products take
@@ -138,15 +158,18 @@ def attend_sequential(ops, a, list4, list8, dV, gV, list16=()):
     path's units (U / (eta delta_c), l / eta); phase 8 accumulates the
     amplified weights Pt/eta and E4M3 codes times the E4M3 V codes; Exit
     converts back (precision-state-conversion equation); phase 16 then
-    accumulates FP16 weights times FP16 values in the common units."""
+    accumulates FP16 weights times FP16 values in the common units. With
+    ``mx`` the 4-bit phase is MXFP4, whose power-of-two block scales the
+    matrix products apply, so it accumulates in the common units."""
     nq = ops.n_a[a]
     d = ops.phases[4][0].shape[2]
     dV = np.asarray(dV, np.float64)
     m = np.full(nq, -np.inf)
     ell = np.zeros(nq)
     U = np.zeros((nq, d))
+    unit4 = 1.0 if mx else FP4_P_SCALE / gV
     if len(list4):
-        U = U * FP4_P_SCALE / gV                                        # into phase-4 units
+        U = U * unit4                                                   # into phase-4 units
         for b in list4:
             S, Vh, quant = _segment(ops, a, [b], 4)
             S, Vh = S[:, 0], Vh[0]
@@ -154,9 +177,9 @@ def attend_sequential(ops, a, list4, list8, dV, gV, list16=()):
             alpha = np.exp(m - m_new)
             Pt = np.exp(S - m_new[:, None])
             ell = ell * alpha + Pt.sum(axis=1)
-            U = U * alpha[:, None] + (quant(Pt) * FP4_P_SCALE) @ (Vh / gV)
+            U = U * alpha[:, None] + (quant(Pt) @ Vh) * unit4
             m = m_new
-        U = U * gV / FP4_P_SCALE                                        # back to common units
+        U = U / unit4                                                   # back to common units
     if len(list8):
         scale = np.where(dV == 0, 0.0, 1.0 / (ETA * np.where(dV == 0, 1.0, dV)))
         U = U * scale[None, :]                                          # Enter

@@ -10,6 +10,12 @@ Paper: appendix "Quantization Formats and Scales".
   channels encode to zero.
 * FP16 Q/K/V (16-bit path, INT8-and-FP16 paragraph): the values cast to
   IEEE half precision, round to nearest even.
+* MXFP4 (a 4-bit alternative that gfx950's matrix cores take natively; not
+  a format of the paper): OCP microscaling with blocks of 32 along the
+  reduction dimension (channels for Q and K, key slots within a block for
+  V), a power-of-two scale X = 2^(floor(log2 max|x|) - 2) clamped to
+  [2^-127, 2^127] (2^-127 for an all-zero block), elements E2M1(x / X)
+  rounded to nearest even with saturation.
 * NVFP4 (NVFP4 quantization equation): E2M1 values with an E4M3 scale per
   group of 16 along the reduction dimension (channels for Q and K, key
   slots within a block for V), a positive per-tensor scale g_X,
@@ -78,6 +84,52 @@ def nvfp4_groups(x, g):
     e = e2m1(f32(x * inv[..., None]))
     e = np.where(zero[..., None], 0.0, e)
     return sigma, e
+
+
+MX_GROUP = 32
+
+
+def mx_scale_exponents(amax):
+    """E8M0 exponents k of the MX blocks: floor(log2 amax) - 2, clamped to
+    [-127, 127]; -127 for a zero block."""
+    amax = np.asarray(amax, dtype=np.float64)
+    _, e = np.frexp(np.where(amax > 0, amax, 1.0))          # amax = f 2^e, f in [0.5, 1)
+    k = (e - 1) - 2
+    return np.where(amax > 0, np.clip(k, -127, 127), -127).astype(np.int64)
+
+
+def mx_groups(x):
+    """MXFP4-encode ``x`` [..., G, 32] (blocks on the last axis). Returns
+    (k [..., G] scale exponents, e [..., G, 32] E2M1 values)."""
+    k = mx_scale_exponents(np.abs(x).max(axis=-1))
+    e = e2m1(np.asarray(x, np.float64) / np.ldexp(1.0, k)[..., None])
+    return k, e
+
+
+def encode_head_mx(Q, K, V, slot2tok, n_a):
+    """MXFP4 operands of one head, slot ordered: kQ, kK [R,64,d/32] and
+    eQ, eK [R,64,d]; kV [R,2,d] (32-slot blocks per channel) and eV [R,64,d]."""
+    Qs, Ks, Vs = (gather_slots(X.astype(np.float32), slot2tok) for X in (Q, K, V))
+    R, _, d = Qs.shape
+    out = {}
+    for name, Xs in (("Q", Qs), ("K", Ks)):
+        k, e = mx_groups(Xs.reshape(R, CAP, d // MX_GROUP, MX_GROUP))
+        out["k" + name], out["e" + name] = k, e.reshape(R, CAP, d)
+    vt = Vs.reshape(R, CAP // MX_GROUP, MX_GROUP, d).transpose(0, 1, 3, 2)   # [R, 2, d, 32]
+    k, e = mx_groups(vt)
+    out["kV"] = k
+    out["eV"] = e.transpose(0, 1, 3, 2).reshape(R, CAP, d)
+    return out
+
+
+def reconstruct_mx(enc):
+    """MXFP4 operands in original units: Qh4/Kh4/Vh4 = 2^k e."""
+    R, _, d = enc["eQ"].shape
+    rec = {}
+    for name in ("Q", "K"):
+        rec[name + "h4"] = np.ldexp(1.0, np.repeat(enc["k" + name], MX_GROUP, axis=2)) * enc["e" + name]
+    rec["Vh4"] = np.ldexp(1.0, np.repeat(enc["kV"], MX_GROUP, axis=1)) * enc["eV"]
+    return rec
 
 
 def encode_head(Q, K, V, slot2tok, n_a, amaxQ=None, amaxK=None, amaxV=None):

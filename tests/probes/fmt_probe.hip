@@ -55,3 +55,32 @@ extern "C" int da2_probe_lds_dma(const uint32_t* src, uint32_t* out, void* strea
   hipLaunchKernelGGL(lds_dma_probe_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, src, out);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
+
+// Scaled fp4 matrix product: one wave computes D = A B with
+// v_mfma_scale_f32_32x32x64_f8f6f4 on E2M1 operands (format 4) for each byte
+// selector 0..3 of the per-lane E8M0 scale words. a, b: 64 lanes x 4 words of
+// packed codes; sa, sb: one scale word per lane; out: [4][64][16] floats in
+// accumulator order.
+typedef int i32x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__global__ void mfma_fp4_probe_kernel(const uint32_t* a, const uint32_t* b, const uint32_t* sa, const uint32_t* sb,
+                                      float* out) {
+  const int l = threadIdx.x;
+  const i32x8_t av = {(int)a[4 * l], (int)a[4 * l + 1], (int)a[4 * l + 2], (int)a[4 * l + 3], 0, 0, 0, 0};
+  const i32x8_t bv = {(int)b[4 * l], (int)b[4 * l + 1], (int)b[4 * l + 2], (int)b[4 * l + 3], 0, 0, 0, 0};
+  const int xa = (int)sa[l], xb = (int)sb[l];
+  f32x16_t d[4];
+  d[0] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, f32x16_t{}, 4, 4, 0, xa, 0, xb);
+  d[1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, f32x16_t{}, 4, 4, 1, xa, 1, xb);
+  d[2] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, f32x16_t{}, 4, 4, 2, xa, 2, xb);
+  d[3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, f32x16_t{}, 4, 4, 3, xa, 3, xb);
+  for (int s = 0; s < 4; ++s)
+    for (int i = 0; i < 16; ++i) out[(s * 64 + l) * 16 + i] = d[s][i];
+}
+
+extern "C" int da2_probe_mfma_fp4(const uint32_t* a, const uint32_t* b, const uint32_t* sa, const uint32_t* sb,
+                                  float* out, void* stream) {
+  hipLaunchKernelGGL(mfma_fp4_probe_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, a, b, sa, sb, out);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}

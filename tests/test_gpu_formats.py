@@ -104,3 +104,48 @@ def test_lds_dma_placement():
     o = out.cpu().numpy()
     assert np.array_equal(o[64:320], src.cpu().numpy())
     assert np.all(o[:64] == -1) and np.all(o[320:] == -1)
+
+
+def test_scaled_fp4_mfma_layout():
+    """v_mfma_scale_f32_32x32x64_f8f6f4 with E2M1 operands: lane l of A holds row
+    l%32 and k = 32(l/32) + i at nibble i (little-endian), lane l of B holds
+    column l%32 with the same k, each lane's E8M0 byte (chosen by the selector)
+    scales its 32 values, and accumulator register i of lane l is row
+    8(i/4) + 4(l/32) + i%4, column l%32 (the layout the MX 4-bit phase uses)."""
+    lib = ctypes.CDLL(PROBE)
+    rng = np.random.default_rng(3)
+    codes_a = rng.integers(0, 16, (64, 32)).astype(np.uint32)
+    codes_b = rng.integers(0, 16, (64, 32)).astype(np.uint32)
+
+    def pack(c):
+        words = np.zeros((64, 4), np.uint32)
+        for i in range(32):
+            words[:, i // 8] |= c[:, i] << (4 * (i % 8))
+        return words
+
+    sa = rng.integers(120, 134, (64, 4)).astype(np.uint32)
+    sb = rng.integers(120, 134, (64, 4)).astype(np.uint32)
+    sa_w = (sa[:, 0] | (sa[:, 1] << 8) | (sa[:, 2] << 16) | (sa[:, 3] << 24)).astype(np.uint32)
+    sb_w = (sb[:, 0] | (sb[:, 1] << 8) | (sb[:, 2] << 16) | (sb[:, 3] << 24)).astype(np.uint32)
+    dev = [torch.from_numpy(x.view(np.int32).copy()).cuda() for x in (pack(codes_a), pack(codes_b), sa_w, sb_w)]
+    out = torch.zeros(4 * 64 * 16, dtype=torch.float32, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    assert lib.da2_probe_mfma_fp4(*[ctypes.c_void_p(t.data_ptr()) for t in dev], ctypes.c_void_p(out.data_ptr()),
+                                  stream) == 0
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().reshape(4, 64, 16)
+    mag = F.E2M1_VALUES
+    val = lambda c: np.where(c & 8, -1.0, 1.0) * mag[c & 7]
+    va, vb = val(codes_a), val(codes_b)
+    for sel in range(4):
+        A = np.zeros((32, 64))
+        B = np.zeros((64, 32))
+        for l in range(64):
+            r, h = l % 32, l // 32
+            A[r, 32 * h:32 * h + 32] = va[l] * 2.0 ** (int(sa[l, sel]) - 127)
+            B[32 * h:32 * h + 32, r] = vb[l] * 2.0 ** (int(sb[l, sel]) - 127)
+        D = A @ B
+        for l in range(64):
+            for i in range(16):
+                row = 8 * (i // 4) + 4 * (l // 32) + i % 4
+                assert got[sel, l, i] == pytest.approx(D[row, l % 32], rel=1e-6, abs=1e-30), (sel, l, i)

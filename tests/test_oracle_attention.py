@@ -248,3 +248,51 @@ def test_fp16_weights_scalar():
     W = att.quant_weights_fp16(Pt)
     for p, w in zip(Pt, W):
         assert w == struct.unpack("e", struct.pack("e", float(p)))[0]
+
+
+def _mx_ops(Q, K, V, layout):
+    slot2tok, n_a, _ = layout
+    enc = encode.encode_head(Q, K, V, slot2tok, n_a)
+    encm = encode.encode_head_mx(Q, K, V, slot2tok, n_a)
+    return enc, att.Operands.quantized(encode.reconstruct(enc), n_a, encode.reconstruct_mx(encm)), encm
+
+
+@pytest.mark.parametrize("lists", [([0, 2, 5], [1, 3], []), ([1, 4], [], [2]), ([0], [3], [1])])
+def test_mx_closed_form_equals_sequential(lists):
+    """With MXFP4 the 4-bit phase accumulates in the common units; the closed
+    form still equals the recurrence with Enter / Exit."""
+    Q, K, V, layout = _case(13, scale=1.5)
+    enc, ops, _ = _mx_ops(Q, K, V, layout)
+    l4, l8, l16 = lists
+    for a in range(layout[1].size):
+        O1 = att.attend(ops, a, l4, l8, l16)
+        O2 = att.attend_sequential(ops, a, l4, l8, enc["dV"], float(enc["gV"]), l16, mx=True)
+        np.testing.assert_allclose(O1, O2, rtol=1e-12, atol=1e-13)
+
+
+def test_mx_equal_logits_give_exact_mean():
+    """Equal logits: every Pt is 1, X = 2^-2, Pt / X = 4 is an E2M1 value, so
+    every MX weight is exactly 1 and O is the mean of the MX values."""
+    Q, K, V, layout = _case(14)
+    Q[:] = 0.0
+    slot2tok, n_a, _ = layout
+    _, ops, encm = _mx_ops(Q, K, V, layout)
+    rec = encode.reconstruct_mx(encm)
+    blocks = [0, 3]
+    kslots = np.concatenate([np.arange(b * 64, b * 64 + n_a[b]) for b in blocks])
+    O = att.attend(ops, 1, blocks, [])
+    mean = rec["Vh4"].reshape(-1, Q.shape[1])[kslots].mean(axis=0)
+    np.testing.assert_allclose(O, np.broadcast_to(mean, O.shape), rtol=1e-13, atol=1e-14)
+
+
+def test_mx_weights_scalar_brute_force():
+    from test_oracle_encode import _mx_brute
+    rng = np.random.default_rng(15)
+    Pt = np.exp(-rng.exponential(3.0, (9, 64)))
+    Pt[0, :32] = 0.0
+    Pt[1, 32:] = 2.0 ** -140                      # below the smallest scale
+    W = att.quant_weights_mx(Pt)
+    for u in range(Pt.shape[0]):
+        for g in range(2):
+            k, e = _mx_brute(Pt[u, 32 * g:32 * g + 32])
+            assert list(W[u, 32 * g:32 * g + 32]) == [2.0 ** k * v for v in e]

@@ -157,3 +157,56 @@ def test_fp16_operands_are_half_casts():
             assert list(got[idx][:4]) == want
         pad = np.arange(64)[None, :] >= n_a[:, None]
         assert np.all(got[pad] == 0)
+
+
+def _mx_brute(block):
+    """OCP MX block of E2M1 elements, scalar Python: X = 2^(floor(log2 amax) - 2)."""
+    import math
+    amax = max(abs(float(v)) for v in block)
+    if amax == 0:
+        return -127, [0.0] * len(block)
+    m, e = math.frexp(amax)            # amax = m 2^e, m in [0.5, 1)
+    k = max(-127, min(127, e - 1 - 2))
+    return k, [e2m1_bf(float(v) / 2.0 ** k) for v in block]
+
+
+def test_mx_scalar_brute_force_and_top_code():
+    """MXFP4 blocks against a scalar transcription of the OCP rule; the block
+    maximum always lands on E2M1 4 or 6 (amax / X in [4, 8), 6 saturating)."""
+    rng = np.random.default_rng(21)
+    X = (rng.standard_normal((40, 32)) * np.exp(rng.uniform(-8, 8, (40, 1)))).astype(np.float32)
+    X[0] = 0.0
+    X[1, :] = 0.0
+    X[1, 5] = -3.0
+    k, e = encode.mx_groups(X.astype(np.float64))
+    for i in range(X.shape[0]):
+        kb, eb = _mx_brute(X[i])
+        assert k[i] == kb
+        assert list(e[i]) == eb
+        if np.abs(X[i]).max() > 0:
+            assert np.abs(e[i]).max() in (4.0, 6.0)
+
+
+def test_mx_head_encoding_layout_and_reconstruction():
+    """Q/K blocks run along channels (32 per token), V blocks along 32 key slots
+    per channel; padding stays zero; |x - x_hat| <= 2X (half the top step is X,
+    saturation of (6, 8) adds at most 2X)."""
+    X, layout = _tiny(7, d=64)
+    slot2tok, n_a, _ = layout
+    enc = encode.encode_head_mx(X, X, X, slot2tok, n_a)
+    rec = encode.reconstruct_mx(enc)
+    Xs = partition.gather_slots(X, slot2tok).astype(np.float64)
+    R = Xs.shape[0]
+    kq, eq = encode.mx_groups(Xs.reshape(R, 64, 2, 32))
+    np.testing.assert_array_equal(enc["kQ"], kq)
+    np.testing.assert_array_equal(rec["Qh4"], np.ldexp(1.0, np.repeat(kq, 32, axis=2)) * eq.reshape(R, 64, 64))
+    for a in range(R):
+        for c in (0, 17, 63):
+            for g in range(2):
+                kb, eb = _mx_brute(Xs[a, 32 * g:32 * g + 32, c])
+                assert enc["kV"][a, g, c] == kb
+                assert list(enc["eV"][a, 32 * g:32 * g + 32, c]) == eb
+    bound_q = 2 * np.ldexp(1.0, np.repeat(enc["kQ"], 32, axis=2))
+    assert np.all(np.abs(rec["Qh4"] - Xs) <= bound_q)
+    pad = np.arange(64)[None, :] >= n_a[:, None]
+    assert np.all(rec["Vh4"][pad] == 0) and np.all(rec["Qh4"][pad] == 0)
