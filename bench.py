@@ -10,14 +10,16 @@ Prints one JSON line. ``value`` is the dense-equivalent throughput of the
 whole step, 4*B*H*N^2*d flops per step; mixed_attn alone is reported too.
 The roofline object covers mixed_attn, the dominant kernel: algorithmic
 flops = retained tiles x 4*64*64*d (8-bit tiles priced at the int8/fp8
-peak, 4-bit tiles at the fp16 peak the NVFP4 path issues), divided by the
+peak, 4-bit tiles at the fp16 peak the NVFP4 path issues, or at the fp4 peak
+with --fmt4 mxfp4), divided by the
 kernel's average duration measured with HIP events on its stream. Its
 ``traffic`` is the HBM bytes per launch that rocprofv3 counted for the same
 kernel source (profiles/mixed_attn_traffic.json, FETCH_SIZE and WRITE_SIZE
 scaled by a plain-copy calibration), or null when the source has changed
 since. The ``hbm`` object rates draft_map and prep_operands against HBM
 bandwidth with the bytes each call must move: draft_map reads Q and K and
-writes A; prep_operands reads Q, K and V and writes the operand buffer.
+writes A; prep_operands reads Q, K and V and writes the operand sections
+that the run uses.
 """
 import argparse
 import hashlib
@@ -36,6 +38,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_8BIT = 5.0e15      # MI355X dense int8 / fp8 MFMA (published)
 PEAK_FP16 = 2.5e15      # MI355X dense fp16 / bf16 MFMA (published)
+PEAK_FP4 = 10.1e15      # MI355X dense fp4 / fp6 MFMA (published)
 PEAK_HBM = 8.0e12       # bytes/s
 TRAFFIC = os.path.join(ROOT, "profiles", "mixed_attn_traffic.json")
 ATTN_SOURCES = [os.path.join(ROOT, "paper_2609_32628_amd", "csrc", f) for f in ("attn.hip", "common.hpp", "launch.hpp")]
@@ -77,6 +80,8 @@ def parse():
                     help="region partition (the configured workloads use 8x8 tiles)")
     ap.add_argument("--num16", type=int, default=None,
                     help="num16/den of the region pairs on the 16-bit path (the hot path uses 0)")
+    ap.add_argument("--fmt4", choices=("nvfp4", "mxfp4"), default="nvfp4",
+                    help="encoding of the 4-bit path: the paper's NVFP4 (default) or gfx950's native MXFP4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 512 MiB device copy (HBM counter calibration)")
@@ -142,9 +147,9 @@ def main():
     def step(ev=None):
         calls = (lambda: api.da2_draft_map(dev[0], dev[1], buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft),
                  lambda: api.da2_rank_assign(buf.A, p, w.num16, *w.budgets, w.scope, buf.cls, buf.lists, buf.ws_rank),
-                 lambda: api.da2_prep_operands(dev[0], dev[1], dev[2], buf.layout, p, int(w.num16 > 0), buf.stats,
-                                               buf.ops, None),
-                 lambda: api.da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O))
+                 lambda: api.da2_prep_operands(dev[0], dev[1], dev[2], buf.layout, p, int(w.num16 > 0), args.fmt4,
+                                               buf.stats, buf.ops, None),
+                 lambda: api.da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, fmt4=args.fmt4))
         for i, c in enumerate(calls):
             if ev is not None:
                 ev[i][0].record(stream)
@@ -185,13 +190,19 @@ def main():
     F8, F4, F16 = n8 * tile_flops, n4 * tile_flops, n16 * tile_flops
     t_attn = stage_ms["mixed_attn"] * 1e-3
     achieved = (F8 + F4 + F16) / t_attn
-    peak_eff = (F8 + F4 + F16) / (F8 / PEAK_8BIT + (F4 + F16) / PEAK_FP16)
+    mx = args.fmt4 == "mxfp4"
+    peak4 = PEAK_FP4 if mx else PEAK_FP16
+    peak_eff = (F8 + F4 + F16) / (F8 / PEAK_8BIT + F4 / peak4 + F16 / PEAK_FP16)
     dense_flops = 4.0 * w.B * w.H * w.N ** 2 * w.d
     # bytes each preparation call must move (bf16 inputs)
     sizes = buf.sizes
     e_in = w.B * w.H * w.N * w.d * 2
     draft_bytes = 2 * e_in + sizes["A_bytes"]
-    prep_bytes = 3 * e_in + sizes["ops_bytes"]
+    # sections prep_operands writes: 8-bit operands and scales, the 4-bit
+    # encoding in use, and the 16-bit operands only when that path is on
+    off = api.da2_ops_offsets(p) + [sizes["ops_bytes"]]
+    written = [3, 4, 5, 6, 7, 8, 9] + ([13, 14, 15] if mx else [0, 1, 2]) + ([10, 11, 12] if w.num16 > 0 else [])
+    prep_bytes = 3 * e_in + sum(off[i + 1] - off[i] for i in written)
     t_draft, t_prep = stage_ms["draft_map"] * 1e-3, stage_ms["prep_operands"] * 1e-3
     hbm = {"draft_map": {"bytes": draft_bytes, "GB/s": draft_bytes / t_draft / 1e9,
                          "frac": draft_bytes / t_draft / PEAK_HBM},
@@ -206,12 +217,14 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "mixed: int8/fp8 + fp16(nvfp4-exact) MFMA, fp32 softmax state; bf16 in/out",
+        "dtype": ("mixed: int8/fp8 + scaled fp4 (mxfp4) MFMA" if mx else
+                  "mixed: int8/fp8 + fp16(nvfp4-exact) MFMA") + ", fp32 softmax state; bf16 in/out",
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "heads": w.H, "tokens": w.N, "d": w.d,
                    "grid": [w.T, w.Hg, w.Wg], "budgets_8_4_skip": [w.budgets[0], w.budgets[1],
                                                                    w.budgets[2] - w.budgets[0] - w.budgets[1] - w.num16],
                    "scope": w.scope, "lambda": w.lam, "num16": w.num16, "partition": w.partition,
+                   "fmt4": args.fmt4,
                    "parallelism": "single GPU"},
         "stage_ms": stage_ms,
         "mixed_attn_ms": stage_ms["mixed_attn"],
@@ -219,10 +232,14 @@ def main():
         "tiles": {"8bit": n8, "4bit": n4, "16bit": n16},
         "roofline": {"bound": "mfma", "kernel": "mixed_attn_kernel", "achieved": achieved / 1e12,
                      "peak": peak_eff / 1e12, "unit": "TFLOP/s", "frac": achieved / peak_eff,
-                     "traffic": recorded_traffic(w.name),
-                     "peak_note": "budget-weighted: 8-bit tiles at 5.0 PF (int8/fp8), 4-bit tiles at 2.5 PF "
-                                  "(fp16 MFMA on exact NVFP4 reconstructions), 16-bit tiles at 2.5 PF",
-                     "frac_vs_fp4_peak": achieved * (F8 / PEAK_8BIT + F4 / 10.0e15 + F16 / PEAK_FP16) / (F8 + F4 + F16)},
+                     # recorded for the workload's own configuration only
+                     "traffic": recorded_traffic(w.name) if args.partition is None and args.num16 is None
+                     and not mx else None,
+                     "peak_note": "budget-weighted: 8-bit tiles at 5.0 PF (int8/fp8), 4-bit tiles at "
+                                  + ("10.1 PF (scaled fp4 MFMA, MXFP4)" if mx else
+                                     "2.5 PF (fp16 MFMA on exact NVFP4 reconstructions)")
+                                  + ", 16-bit tiles at 2.5 PF",
+                     "frac_vs_fp4_peak": achieved * (F8 / PEAK_8BIT + F4 / PEAK_FP4 + F16 / PEAK_FP16) / (F8 + F4 + F16)},
         "hbm": hbm,
     }
     if not args.no_cpu_baseline:

@@ -7,7 +7,8 @@
  *
  *   da2_draft_map      pooled draft attention map            (descriptor eq., Def. 3.1)
  *   da2_rank_assign    shared ranking into 16/8/4-bit or skip (Algorithm 1, routing appendix)
- *   da2_prep_operands  per-block INT8 / E4M3 / NVFP4 operands (format appendix, NVFP4 eqs.)
+ *   da2_prep_operands  per-block INT8 / E4M3 / NVFP4 (or MXFP4) operands (format appendix,
+ *                      NVFP4 eqs.)
  *   da2_mixed_attn     one phased mixed-precision attention   (phased execution,
  *                      kernel with shared softmax state       precision-state-conversion eq.)
  *
@@ -63,6 +64,13 @@ typedef enum {
 
 typedef enum { DA2_BF16 = 0, DA2_FP32 = 1 } da2_dtype;
 typedef enum { DA2_SCOPE_HEAD = 0, DA2_SCOPE_ROW = 1 } da2_scope;
+
+/* Encodings of the 4-bit path. NVFP4 is the paper's format (E2M1 with an
+ * E4M3 scale per 16 elements and a per-tensor scale). MXFP4 is the OCP
+ * microscaling format that gfx950's matrix cores apply natively (E2M1 with a
+ * power-of-two E8M0 scale per 32 elements); it is a hardware counterpart of
+ * the paper's 4-bit path, not a format of the paper. */
+typedef enum { DA2_FMT4_NVFP4 = 0, DA2_FMT4_MXFP4 = 1 } da2_fmt4;
 
 /* Region partitions of each frame (capacity C = 64 slots per block). */
 typedef enum {
@@ -182,15 +190,24 @@ int32_t da2_lists_offsets(const da2_problem* p, int64_t* offsets4);
  *     bits, so fp16 holds it exactly and fp16 MFMA reproduces the products).
  *   FP16 Q, K, V (16-bit path, INT8 and FP16 paragraph): the values rounded
  *     to nearest-even half precision; written only when with16 = 1.
+ *   MXFP4 Q, K (32-channel blocks) and V (32 key slots per channel), written
+ *     instead of NVFP4 when fmt4 = DA2_FMT4_MXFP4: k = floor(log2 amax_G) - 2
+ *     clamped to [-127, 127] (-127 for an all-zero block), e =
+ *     E2M1_rne(x * 2^-k) (exact scaling), stored as 4-bit codes with the
+ *     E8M0 byte k + 127.
  * Casts round to nearest even and saturate; padding slots encode to zero.
  *   Q, K, V  device [B,H,N,d] per *qkv; stats from da2_draft_map (this call
  *            fills entries 2.. : max|V| and the per-channel max|V_c|)
  *   with16   0 or 1: also write the 16-bit sections [10..12] of ops. A
  *            da2_mixed_attn call whose lists hold 16-bit blocks needs them.
- *   ops      device out, ops_bytes (see da2_ops_offsets)                   */
+ *   fmt4     da2_fmt4: NVFP4 writes sections [0..2], MXFP4 sections
+ *            [13..15]; the other 4-bit sections are left untouched, and
+ *            da2_mixed_attn must be called with the same fmt4.
+ *   ops      device out, ops_bytes (see da2_ops_offsets)
+ * Errors: INVALID_ARG for with16 or fmt4 out of range, misaligned inputs.   */
 int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv,
-                          const int32_t* layout, const da2_problem* p, int32_t with16, void* stats,
-                          void* ops, void* ws, int64_t ws_bytes, void* stream);
+                          const int32_t* layout, const da2_problem* p, int32_t with16, int32_t fmt4,
+                          void* stats, void* ops, void* ws, int64_t ws_bytes, void* stream);
 
 /* Offsets (bytes) inside ops, per section; each section is [B*H][R][...]
  * with one 64-slot block per R, in the fragment order of the gfx950 MFMA
@@ -207,10 +224,22 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
  *   [9] g   float32 [B*H][4]   (g_Q, g_K, g_V, 0) NVFP4 tensor scales
  *   [10] Q16, [11] K16, [12] V16  fp16, the layouts of Q4, K4, V4 holding the
  *            half-precision values of the 16-bit path
+ *   [13] Q4mx, [14] K4mx, [15] V4mx  MXFP4 operands, (d/32 + 1) fragments of
+ *            1 KB per block: d/32 data fragments, then one scale fragment.
+ *            Code i (0..31) of a lane sits in byte i/2 of the lane's 16 bytes,
+ *            low nibble first (sign bit 3).
+ *     Q4mx data [qt:2][s:d/64][lane][32 codes] = Q[slot 32qt+lane%32][64s+32g+i]
+ *     K4mx data [j:2][s:d/64][lane][32 codes]  = K[kappa_mx(j,lane%32)][64s+32g+i]
+ *     V4mx data [t:d/32][lane][32 codes]       = V[32g+i][32t+lane%32]
+ *     scale fragment: uint32 [lane][4], word w = 127 + k of the block that
+ *     the lane's codes in data fragment w belong to (w = qt*(d/64)+s, j*(d/64)+s
+ *     or t); unused words are 0.
  * with kappa(j, r) = 32j + 16((r/4)%2) + 4(r/8) + r%4 (the key permutation
  * that puts each 16-slot group of a query row into one lane, see the operand
- * permutation equation). */
-int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets13);
+ * permutation equation) and kappa_mx(j, r) = 32((r/4)%2) + 16j + 4(r/8) + r%4
+ * (the one that puts each 32-slot MXFP4 block of a query row into one lane
+ * half). */
+int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets16);
 
 /* Phased mixed-precision attention (phased-execution appendix;
  * precision-state-conversion equation). For each query block a (one
@@ -226,12 +255,20 @@ int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets13);
  *   Exit:  U_c *= eta delta_c, l *= eta
  *   16-bit: fp16 MFMA logits; Pt = exp(s - m); l += sum Pt; U += fp16(Pt) V16
  *   O = U / l (0 if no retained block)
- * and the rows are written to token order through slot2tok.
+ * and the rows are written to token order through slot2tok. With fmt4 =
+ * DA2_FMT4_MXFP4 the 4-bit phase runs on the MXFP4 sections instead:
+ *   4-bit: scaled fp4 MFMA logits; l += sum Pt; per query and 32-slot block
+ *          k = floor(log2 max Pt) - 2 (clamped at -127); U += 2^k
+ *          E2M1(Pt 2^-k) Vhat4 (scaled fp4 MFMA), already in the common units
+ *          (no factor g_V/2688 to restore).
  *   ops, lists, layout  device, from the calls above
+ *   fmt4     da2_fmt4 used by da2_prep_operands for these ops
  *   out      descriptor of O (dtype fp32 or bf16)
- *   O        device out [B,H,N,d]; every token row is written.               */
+ *   O        device out [B,H,N,d]; every token row is written.
+ * Errors: INVALID_ARG for fmt4 out of range or a bad descriptor.           */
 int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout,
-                       const da2_problem* p, const da2_tensor* out, void* O, void* stream);
+                       const da2_problem* p, int32_t fmt4, const da2_tensor* out, void* O,
+                       void* stream);
 
 #ifdef __cplusplus
 }

@@ -9,9 +9,10 @@ import numpy as np
 from . import attention, draft, encode, partition, rank
 
 
-def run_head(Q, K, V, layout, lam, budgets, scope, rows=None, mode="quant", num16=0):
+def run_head(Q, K, V, layout, lam, budgets, scope, rows=None, mode="quant", num16=0, fmt4="nvfp4"):
     """One (batch, head). Q, K, V: [N, d] float32 values; budgets
-    (num8, num4, den) plus num16/den for the 16-bit path.
+    (num8, num4, den) plus num16/den for the 16-bit path; fmt4 selects the
+    4-bit encoding ("nvfp4" or "mxfp4").
 
     ``rows`` restricts the attention to a subset of query regions (the draft,
     ranking and encodings always cover the whole head). Returns a dict with
@@ -20,8 +21,10 @@ def run_head(Q, K, V, layout, lam, budgets, scope, rows=None, mode="quant", num1
     A32, pooled = draft.draft_head(Q, K, slot2tok, n_a, lam)
     cls = rank.rank_head(A32, *budgets, scope, num16=num16)
     enc = encode.encode_head(Q, K, V, slot2tok, n_a)
+    enc_mx = encode.encode_head_mx(Q, K, V, slot2tok, n_a) if fmt4 == "mxfp4" else None
     if mode == "quant":
-        ops = attention.Operands.quantized(encode.reconstruct(enc), n_a)
+        rec_mx = None if enc_mx is None else encode.reconstruct_mx(enc_mx)
+        ops = attention.Operands.quantized(encode.reconstruct(enc), n_a, rec_mx)
     else:
         ops = attention.Operands.exact(*(partition.gather_slots(X, slot2tok) for X in (Q, K, V)), n_a)
     R = n_a.size
@@ -30,7 +33,7 @@ def run_head(Q, K, V, layout, lam, budgets, scope, rows=None, mode="quant", num1
         l4, l8, l16 = rank.key_lists_all(cls[a])
         toks = slot2tok[a * partition.CAP: a * partition.CAP + n_a[a]]
         O[toks] = attention.attend(ops, a, l4, l8, l16)
-    return dict(A32=A32, pooled=pooled, cls=cls, enc=enc, O=O)
+    return dict(A32=A32, pooled=pooled, cls=cls, enc=enc, enc_mx=enc_mx, O=O)
 
 
 def run(w, Q, K, V, heads=None, rows=None, mode="quant"):
@@ -40,5 +43,5 @@ def run(w, Q, K, V, heads=None, rows=None, mode="quant"):
     for b in range(Q.shape[0]):
         for h in (range(Q.shape[1]) if heads is None else heads):
             out.append(run_head(Q[b, h], K[b, h], V[b, h], layout, w.lam, w.budgets,
-                                w.scope, rows=rows, mode=mode, num16=w.num16))
+                                w.scope, rows=rows, mode=mode, num16=w.num16, fmt4=w.fmt4))
     return layout, out

@@ -13,6 +13,7 @@ DA2_OK, DA2_ERR_INVALID_ARG, DA2_ERR_UNSUPPORTED, DA2_ERR_WORKSPACE, DA2_ERR_HIP
 DA2_BF16, DA2_FP32 = 0, 1
 DA2_SCOPE_HEAD, DA2_SCOPE_ROW = 0, 1
 DA2_PART_TILES8, DA2_PART_RAGGED = 0, 1
+DA2_FMT4_NVFP4, DA2_FMT4_MXFP4 = 0, 1
 
 # Every symbol include/da2.h declares.
 EXPORTS = ("da2_status_string", "da2_sizes", "da2_layout_build", "da2_draft_map", "da2_ws_draft_offsets",
@@ -66,9 +67,9 @@ def lib():
             "da2_ws_draft_offsets": (i32, [P, pi64]),
             "da2_rank_assign": (i32, [vp, P, i32, i32, i32, i32, i32, vp, vp, vp, i64, vp]),
             "da2_lists_offsets": (i32, [P, pi64]),
-            "da2_prep_operands": (i32, [vp, vp, vp, T, vp, P, i32, vp, vp, vp, i64, vp]),
+            "da2_prep_operands": (i32, [vp, vp, vp, T, vp, P, i32, i32, vp, vp, vp, i64, vp]),
             "da2_ops_offsets": (i32, [P, pi64]),
-            "da2_mixed_attn": (i32, [vp, vp, vp, P, T, vp, vp]),
+            "da2_mixed_attn": (i32, [vp, vp, vp, P, i32, T, vp, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)

@@ -12,11 +12,12 @@ import numpy as np
 import torch
 
 from . import _lib
-from ._lib import (DA2_BF16, DA2_FP32, DA2_PART_RAGGED, DA2_PART_TILES8, DA2_SCOPE_HEAD, DA2_SCOPE_ROW, Problem,
-                   Tensor, check, lib)
+from ._lib import (DA2_BF16, DA2_FMT4_MXFP4, DA2_FMT4_NVFP4, DA2_FP32, DA2_PART_RAGGED, DA2_PART_TILES8,
+                   DA2_SCOPE_HEAD, DA2_SCOPE_ROW, Problem, Tensor, check, lib)
 
 SCOPES = {"head": DA2_SCOPE_HEAD, "row": DA2_SCOPE_ROW}
 PARTITIONS = {"tiles8": DA2_PART_TILES8, "ragged": DA2_PART_RAGGED}
+FMT4 = {"nvfp4": DA2_FMT4_NVFP4, "mxfp4": DA2_FMT4_MXFP4}
 
 
 def problem(B, H, d, T, Hg, Wg, partition="tiles8"):
@@ -71,7 +72,7 @@ def da2_lists_offsets(p):
 
 
 def da2_ops_offsets(p):
-    return _offsets("da2_ops_offsets", p, 13)
+    return _offsets("da2_ops_offsets", p, 16)
 
 
 def da2_draft_map(Q, K, layout, p, lam, A, stats, ws, stream=None):
@@ -86,18 +87,18 @@ def da2_rank_assign(A, p, num16, num8, num4, den, scope, cls, lists, ws, stream=
         ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def da2_prep_operands(Q, K, V, layout, p, with16, stats, ops, ws, stream=None):
+def da2_prep_operands(Q, K, V, layout, p, with16, fmt4, stats, ops, ws, stream=None):
     if not (Q.shape == K.shape == V.shape and Q.stride() == K.stride() == V.stride() and Q.dtype == K.dtype == V.dtype):
         raise ValueError("Q, K and V must share shape, strides and dtype")
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     check("da2_prep_operands", lib().da2_prep_operands(
         _ptr(Q), _ptr(K), _ptr(V), ctypes.byref(_tensor_desc(Q)), _ptr(layout), ctypes.byref(p), int(with16),
-        _ptr(stats), _ptr(ops), None if ws is None else _ptr(ws), ws_bytes, _stream(stream)))
+        FMT4[fmt4], _ptr(stats), _ptr(ops), None if ws is None else _ptr(ws), ws_bytes, _stream(stream)))
 
 
-def da2_mixed_attn(ops, lists, layout, p, O, stream=None):
+def da2_mixed_attn(ops, lists, layout, p, O, stream=None, fmt4="nvfp4"):
     check("da2_mixed_attn", lib().da2_mixed_attn(
-        _ptr(ops), _ptr(lists), _ptr(layout), ctypes.byref(p), ctypes.byref(_tensor_desc(O)), _ptr(O),
+        _ptr(ops), _ptr(lists), _ptr(layout), ctypes.byref(p), FMT4[fmt4], ctypes.byref(_tensor_desc(O)), _ptr(O),
         _stream(stream)))
 
 
@@ -133,12 +134,13 @@ def alloc(p, scope="head", device="cuda"):
                    ws_draft=raw(s["ws_draft_bytes"]), ws_rank=raw(s["ws_rank_bytes"]))
 
 
-def attention(Q, K, V, buf, lam, budgets, O, stream=None, num16=0):
+def attention(Q, K, V, buf, lam, budgets, O, stream=None, num16=0, fmt4="nvfp4"):
     """The four calls in order: draft map, ranking, operand preparation,
-    attention. budgets = (num8, num4, den); num16/den go to the 16-bit path."""
+    attention. budgets = (num8, num4, den); num16/den go to the 16-bit path;
+    fmt4 ("nvfp4" or "mxfp4") is the encoding of the 4-bit path."""
     p = buf.p
     da2_draft_map(Q, K, buf.layout, p, lam, buf.A, buf.stats, buf.ws_draft, stream)
     da2_rank_assign(buf.A, p, num16, *budgets, buf.scope, buf.cls, buf.lists, buf.ws_rank, stream)
-    da2_prep_operands(Q, K, V, buf.layout, p, int(num16 > 0), buf.stats, buf.ops, None, stream)
-    da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, stream)
+    da2_prep_operands(Q, K, V, buf.layout, p, int(num16 > 0), fmt4, buf.stats, buf.ops, None, stream)
+    da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, stream, fmt4)
     return O

@@ -17,8 +17,9 @@
 // registers then feed the P^T operand of O^T with V rows in the matching order
 // (the operand permutation equation (P Pi)(Pi^T V) = P V).
 //
-// Units: the 4-bit phase multiplies fp16 sigma*e operands, so U carries a factor
-// 2688/g_V and l the unamplified weights; Enter converts to the 8-bit path's
+// Units: the NVFP4 phase multiplies fp16 sigma*e operands, so U carries a
+// factor 2688/g_V and l the unamplified weights (the MXFP4 alternative of the
+// 4-bit phase runs scaled fp4 MFMAs and stays in the common units); Enter converts to the 8-bit path's
 // units U_c / (eta delta_c), l / eta; the 8-bit phase accumulates amplified
 // weights 2^(z - m + 8.807) and E4M3 codes; Exit converts back; the 16-bit
 // phase then accumulates fp16 weights times fp16 values in the common units.
@@ -173,6 +174,41 @@ __device__ inline f16x8 half_weights8(const f32x16& S, float c, float mn, float&
   return h;
 }
 
+// MXFP4 path: D += A B on one 32x32x64 scaled fp4 MFMA. a, b: 32 E2M1 codes
+// per lane (k = 32 (lane/32) + i in nibble i); sa, sb: the lanes' E8M0 scale
+// words (byte 0 applies to the lane's 32 codes).
+__device__ inline f32x16 mfma_fp4(const i32x4& a, const i32x4& b, const f32x16& c, int sa, int sb) {
+  const i32x8 a8 = {a[0], a[1], a[2], a[3], 0, 0, 0, 0};
+  const i32x8 b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, sa, 0, sb);
+}
+
+// E8M0 exponent of this lane's 32-slot weight block: floor(log2 max Pt) - 2,
+// clamped below at -127, where max Pt = 2^(gm c - mn) comes from the block's
+// largest logit gm with the same product as the running maximum, so the block
+// that holds the row maximum gets max Pt = 1 exactly.
+__device__ inline int mx_weight_exponent(float gm, float c, float mn) {
+  const float pmax = exp2_fast(gm * c - mn);
+  return max((int)(__float_as_uint(pmax) >> 23) - 129, -127);
+}
+
+// MXFP4 weights of 8 logits S[I0..I0+8): y = Pt 2^-k = 2^(S c + off) with
+// off = -mn - k (added to sum), as E2M1 codes in one dword (value e in nibble e).
+template <int I0>
+__device__ inline int mx_codes8(const f32x16& S, float c, float off, float& sum) {
+  float y[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    y[e] = exp2_fast(__builtin_fmaf(S[I0 + e], c, off));
+    sum += y[e];
+  }
+  uint32_t w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[2], y[3], 1.0f, 1);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[4], y[5], 1.0f, 2);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[6], y[7], 1.0f, 3);
+  return static_cast<int>(w);
+}
+
 // Scheduling fence: no instruction moves across it, so the stages between two
 // fences keep the interleaving of matrix and vector work written in the source.
 __device__ inline void fence() { __builtin_amdgcn_sched_barrier(0); }
@@ -183,6 +219,17 @@ __device__ inline void mask_tail(f32x16 (&S)[2], int nb, int g) {
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int valid = nb - 32 * j - 16 * g;  // valid registers of this lane
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i >= valid) S[j][i] = -INFINITY;
+  }
+}
+
+// The same for the MXFP4 key order: register i of tile j holds slot 32g + 16j + i.
+__device__ inline void mask_tail_mx(f32x16 (&S)[2], int nb, int g) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int valid = nb - 32 * g - 16 * j;
 #pragma unroll
     for (int i = 0; i < 16; ++i)
       if (i >= valid) S[j][i] = -INFINITY;
@@ -220,11 +267,28 @@ __device__ inline float lane_value(float v, int lane) {
 template <int N>
 __device__ inline void wait_vmem_keep() {
   if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (N == 1) asm volatile("s_waitcnt vmcnt(1)" ::: "memory");
   else if constexpr (N == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+  else if constexpr (N == 3) asm volatile("s_waitcnt vmcnt(3)" ::: "memory");
   else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
   else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
   else static_assert(N == 0, "unsupported count");
 }
+// Waits until only the fragments of the most recent tile copy that this wave
+// issued are in flight: NFK/2 each for even NFK; for odd NFK wave 0 copies
+// (NFK+1)/2 fragments and wave 1 the rest.
+template <int NFK>
+__device__ inline void wait_keep_tile(int wave) {
+  if constexpr (NFK % 2 == 0) {
+    wait_vmem_keep<NFK / 2>();
+  } else {
+    if (wave == 0)
+      wait_vmem_keep<(NFK + 1) / 2>();
+    else
+      wait_vmem_keep<NFK / 2>();
+  }
+}
+
 // Workgroup barrier without the memory fences of __syncthreads (the waits
 // above make LDS contents ready; the fences would also drain in-flight DMA).
 __device__ inline void wg_barrier() {
@@ -257,11 +321,19 @@ template <int NFK, typename Frag, typename SA, typename FIRST, typename STEP1, t
 __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_a, const float* dKh,
                                   const Frag* Kh, const Frag* Vh, Frag* sK, Frag* sV, int wave, int lane,
                                   FIRST first_qk, STEP1 region1, STEP2 region2, PV pv) {
-  constexpr int TILE = NFK * 64;  // fragments per tile
-  constexpr int HALF = NFK / 2;   // fragments each wave copies
+  constexpr int TILE = NFK * 64;       // fragments per tile
+  constexpr int W0 = (NFK + 1) / 2;    // fragments wave 0 copies; wave 1 copies the rest
   auto dma_tile = [&](const Frag* src, Frag* dst) {
+    if constexpr (NFK % 2 == 0) {
 #pragma unroll
-    for (int f = wave * HALF; f < (wave + 1) * HALF; ++f) dma_fragment(src + f * 64 + lane, dst + f * 64);
+      for (int f = wave * W0; f < (wave + 1) * W0; ++f) dma_fragment(src + f * 64 + lane, dst + f * 64);
+    } else {
+#pragma unroll
+      for (int i = 0; i < W0; ++i) {
+        const int f = wave ? W0 + i : i;
+        if (f < NFK) dma_fragment(src + f * 64 + lane, dst + f * 64);
+      }
+    }
   };
   KeyWin win = key_window(list, 0, n, n_a, dKh, lane);
   // key block of list entry e, first being the current window's first entry
@@ -292,7 +364,7 @@ __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_
     // K(i+1) copied (V(i), issued later, may still be in flight). On the last
     // block the logits of the region are computed from the unchanged tile and
     // not used.
-    wait_vmem_keep<HALF>();
+    wait_keep_tile<NFK>(wave);
     wg_barrier();
     if (nb < kCap)
       region1.template operator()<true>(Sc, Sn, nb, dk);
@@ -303,7 +375,7 @@ __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_
     if (more2) dma_tile(Kh + (int64_t)kb2 * TILE, sK);
     region2(Sc);  // returns after its results exist, so the wait below stays after it
     if (more2)
-      wait_vmem_keep<HALF>();  // V(i) copied, K(i+2) may still be in flight
+      wait_keep_tile<NFK>(wave);  // V(i) copied, K(i+2) may still be in flight
     else
       wait_vmem_keep<0>();
     wg_barrier();
@@ -348,9 +420,10 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
   for (int t = 0; t < NT; ++t) U[t] = f32x16{};
   float m = -INFINITY, l = 0.0f;
   const float gV = args.g[bh * 4 + 2];
+  const bool mx = args.fmt4 == DA2_FMT4_MXFP4;
 
   // ------------------------------ NVFP4 phase ------------------------------
-  if (n4 > 0) {
+  if (n4 > 0 && !mx) {
     const float c4 = args.g[bh * 4 + 0] * args.g[bh * 4 + 1] * kLog2e * rsqd;
     f16x8 Qf[NS16];
     const f16x8* Qa = reinterpret_cast<const f16x8*>(args.Q4) + (blk0 + a) * (kCap * D / 8);
@@ -441,6 +514,97 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
                                  qk, region1, region2, pv);
   }
 
+  // ------------------------------ MXFP4 phase ------------------------------
+  // The scaled MFMAs apply the E8M0 block scales of both operands, so logits
+  // and numerator are in the common units. Key rows follow kappa_mx: lane half
+  // g of both logit tiles holds the 32-slot block 32g + [0, 32) (register i of
+  // tile j: slot 32g + 16j + i), which is also the k order of the value
+  // product, so each lane quantizes one whole weight block of its query.
+  if (n4 > 0 && mx) {
+    constexpr int NS64 = D / 64, NFM = D / 32 + 1;  // fragments per tile: data, then scales
+    const float c4 = kLog2e * rsqd;
+    const i32x4* Qa = reinterpret_cast<const i32x4*>(args.Q4mx) + (blk0 + a) * (NFM * 64);
+    i32x4 Qf[NS64];
+    int qsc[NS64];
+    const i32x4 qsw = Qa[2 * NS64 * 64 + lane];
+#pragma unroll
+    for (int s = 0; s < NS64; ++s) {
+      Qf[s] = Qa[(qt * NS64 + s) * 64 + lane];
+      qsc[s] = qt ? qsw[NS64 + s] : qsw[s];
+    }
+    i32x4* sKm = reinterpret_cast<i32x4*>(sK);
+    i32x4* sVm = reinterpret_cast<i32x4*>(sV);
+    i32x4 P;
+    int psc = 0;
+    float alpha = 1.0f;
+    typedef f32x16 SA[2];
+    auto qk = [&](SA& S) {
+      const i32x4 ksw = sKm[2 * NS64 * 64 + lane];
+      S[0] = S[1] = f32x16{};
+#pragma unroll
+      for (int s = 0; s < NS64; ++s)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          S[j] = mfma_fp4(sKm[(j * NS64 + s) * 64 + lane], Qf[s], S[j], ksw[j * NS64 + s], qsc[s]);
+    };
+    // Softmax state of the current block, shared by the two regions.
+    float off = 0.0f, sum = 0.0f;
+    int ke = 0;
+    // Region 1: logits of the next block (NS64 stages of two MFMAs) with the
+    // maxima, the block exponent and the first half of the weights.
+    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float) {
+      if constexpr (MASK) mask_tail_mx(Sc, nb, g);
+      const i32x4 ksw = sKm[2 * NS64 * 64 + lane];
+      i32x4 k0 = sKm[lane], k1 = sKm[NS64 * 64 + lane];
+      constexpr int NP = 2;
+#pragma unroll
+      for (int s = 0; s < NS64; ++s) {
+        i32x4 n0 = k0, n1 = k1;
+        if (s + 1 < NS64) {
+          n0 = sKm[(s + 1) * 64 + lane];
+          n1 = sKm[(NS64 + s + 1) * 64 + lane];
+        }
+        Sn[0] = mfma_fp4(k0, Qf[s], s == 0 ? f32x16{} : Sn[0], ksw[s], qsc[s]);
+        Sn[1] = mfma_fp4(k1, Qf[s], s == 0 ? f32x16{} : Sn[1], ksw[NS64 + s], qsc[s]);
+#pragma unroll
+        for (int piece = 0; piece < NP; ++piece) {
+          if (piece * NS64 / NP != s) continue;
+          if (piece == 0) {
+            const float gm = fmaxf(max16(Sc[0]), max16(Sc[1]));  // this lane's block
+            const float mn = new_max(gm, c4, m, l, alpha);
+            ke = mx_weight_exponent(gm, c4, mn);
+            off = -mn - (float)ke;
+          } else {
+            sum = 0.0f;
+            P[0] = mx_codes8<0>(Sc[0], c4, off, sum);
+            P[1] = mx_codes8<8>(Sc[0], c4, off, sum);
+          }
+        }
+        fence();
+        k0 = n0;
+        k1 = n1;
+      }
+    };
+    // Region 2: the second half of the weights, the scale word and l.
+    auto region2 = [&](SA& Sc) {
+      P[2] = mx_codes8<0>(Sc[1], c4, off, sum);
+      P[3] = mx_codes8<8>(Sc[1], c4, off, sum);
+      psc = ke + 127;
+      l += __builtin_amdgcn_ldexpf(sum, ke);  // Pt = 2^k y, exact scaling
+      after(P), after(l), after(psc);
+    };
+    // U += V^T P^T: one scaled MFMA per channel tile.
+    auto pv = [&]() {
+      if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+      const i32x4 vsw = sVm[NT * 64 + lane];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) U[t] = mfma_fp4(sVm[t * 64 + lane], P, U[t], vsw[t], psc);
+    };
+    phase_loop<NFM, i32x4, SA>(keys, n4, L.n_a, dKh, reinterpret_cast<const i32x4*>(args.K4mx) + blk0 * (NFM * 64),
+                               reinterpret_cast<const i32x4*>(args.V4mx) + blk0 * (NFM * 64), sKm, sVm, wave, lane,
+                               qk, region1, region2, pv);
+  }
+
   // per-lane channel of accumulator register i of channel tile t
   auto chan = [&](int t, int i) { return 32 * t + 8 * (i >> 2) + 4 * g + (i & 3); };
   const float eta = exp2_fast(-kExpOffset);
@@ -450,7 +614,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
   if (n8 > 0) {
     // Enter: U_c <- U_c / (eta delta_c), l <- l / eta (after restoring the 4-bit
     // phase's factor g_V/2688).
-    const float restore = n4 > 0 ? gV / 2688.0f : 1.0f;
+    const float restore = n4 > 0 && !mx ? gV / 2688.0f : 1.0f;
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -552,7 +716,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
 #pragma unroll
       for (int i = 0; i < 16; ++i) U[t][i] *= eta * dV[chan(t, i)];
     l *= eta;
-  } else if (n4 > 0) {
+  } else if (n4 > 0 && !mx) {
     const float restore = gV / 2688.0f;
 #pragma unroll
     for (int t = 0; t < NT; ++t) U[t] *= restore;

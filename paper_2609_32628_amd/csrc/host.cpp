@@ -48,6 +48,11 @@ int32_t derive(const da2_problem* p, Dims* o) {
   return DA2_OK;
 }
 
+// MXFP4 section bytes per block: d/32 data fragments and one scale fragment of 1 KB.
+inline int64_t mx_block_bytes(const Dims& d) { return 1024 * (d.d / 32 + 1); }
+
+constexpr int kSections = 16;
+
 void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
   std::memset(s, 0, sizeof(*s));
   s->R = (int32_t)d.R;
@@ -59,7 +64,7 @@ void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
   s->lists_bytes = align_up(2 * d.BH * d.R * d.R) + align_up(16 * d.BH * d.R) + align_up(4 * d.BH * d.R) + kAlign;
   const int64_t e = d.BH * d.Npad * d.d;
   s->ops_bytes = 3 * align_up(2 * e) + 3 * align_up(e) + 2 * align_up(4 * d.BH * d.R) + align_up(4 * d.BH * d.d) +
-                 align_up(16 * d.BH) + 3 * align_up(2 * e);
+                 align_up(16 * d.BH) + 3 * align_up(2 * e) + 3 * align_up(mx_block_bytes(d) * d.BH * d.R);
   s->ws_draft_bytes = 4 * align_up(8 * d.BH * d.R * d.d) + 2 * align_up(8 * d.BH * d.R * d.R);
   int64_t thr = scope == DA2_SCOPE_ROW ? 8 * da2::kCuts * d.BH * d.R : 8 * da2::kCuts * d.BH;
   s->ws_rank_bytes = align_up(4 * d.BH * da2::kCuts * 2048) + align_up(thr) + align_up(8 * da2::kCuts * d.BH) +
@@ -70,9 +75,10 @@ void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
 void ops_offsets(const Dims& d, int64_t* off) {
   const int64_t e = d.BH * d.Npad * d.d;
   int64_t o = 0;
-  const int64_t sz[13] = {2 * e, 2 * e, 2 * e, e, e, e, 4 * d.BH * d.R, 4 * d.BH * d.R, 4 * d.BH * d.d, 16 * d.BH,
-                          2 * e, 2 * e, 2 * e};
-  for (int i = 0; i < 13; ++i) {
+  const int64_t mx = mx_block_bytes(d) * d.BH * d.R;
+  const int64_t sz[kSections] = {2 * e, 2 * e, 2 * e, e, e, e, 4 * d.BH * d.R, 4 * d.BH * d.R, 4 * d.BH * d.d,
+                                 16 * d.BH, 2 * e, 2 * e, 2 * e, mx, mx, mx};
+  for (int i = 0; i < kSections; ++i) {
     off[i] = o;
     o += align_up(sz[i]);
   }
@@ -351,8 +357,8 @@ int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int
 }
 
 int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv, const int32_t* layout,
-                          const da2_problem* p, int32_t with16, void* stats, void* ops, void* ws, int64_t ws_bytes,
-                          void* stream) {
+                          const da2_problem* p, int32_t with16, int32_t fmt4, void* stats, void* ops, void* ws,
+                          int64_t ws_bytes, void* stream) {
   Dims d;
   int32_t st = derive(p, &d);
   if (st) return st;
@@ -360,14 +366,16 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
   if (!Q || !K || !V || !layout || !stats || !ops) return DA2_ERR_INVALID_ARG;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V)) return DA2_ERR_INVALID_ARG;
   if (with16 != 0 && with16 != 1) return DA2_ERR_INVALID_ARG;
+  if (fmt4 != DA2_FMT4_NVFP4 && fmt4 != DA2_FMT4_MXFP4) return DA2_ERR_INVALID_ARG;
   (void)ws;
   if (ws_bytes < 0) return DA2_ERR_WORKSPACE;
   if ((st = check_device())) return st;
-  int64_t off[13];
+  int64_t off[kSections];
   ops_offsets(d, off);
   char* ob = static_cast<char*>(ops);
   da2::PrepArgs a{};
   a.with16 = with16;
+  a.fmt4 = fmt4;
   a.Q = Q;
   a.K = K;
   a.V = V;
@@ -396,18 +404,22 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
   a.Q16 = reinterpret_cast<_Float16*>(ob + off[10]);
   a.K16 = reinterpret_cast<_Float16*>(ob + off[11]);
   a.V16 = reinterpret_cast<_Float16*>(ob + off[12]);
+  a.Q4mx = reinterpret_cast<uint8_t*>(ob + off[13]);
+  a.K4mx = reinterpret_cast<uint8_t*>(ob + off[14]);
+  a.V4mx = reinterpret_cast<uint8_t*>(ob + off[15]);
   return hip_status(da2::launch_prep(a, static_cast<hipStream_t>(stream)));
 }
 
-int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout, const da2_problem* p,
+int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout, const da2_problem* p, int32_t fmt4,
                        const da2_tensor* out, void* O, void* stream) {
   Dims d;
   int32_t st = derive(p, &d);
   if (st) return st;
   if ((st = check_tensor(out, d, true))) return st;
   if (!ops || !lists || !layout || !O) return DA2_ERR_INVALID_ARG;
+  if (fmt4 != DA2_FMT4_NVFP4 && fmt4 != DA2_FMT4_MXFP4) return DA2_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
-  int64_t off[13], lo[4];
+  int64_t off[kSections], lo[4];
   ops_offsets(d, off);
   lists_offsets(d, lo);
   const char* ob = static_cast<const char*>(ops);
@@ -426,6 +438,10 @@ int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout
   a.Q16 = reinterpret_cast<const _Float16*>(ob + off[10]);
   a.K16 = reinterpret_cast<const _Float16*>(ob + off[11]);
   a.V16 = reinterpret_cast<const _Float16*>(ob + off[12]);
+  a.Q4mx = reinterpret_cast<const uint8_t*>(ob + off[13]);
+  a.K4mx = reinterpret_cast<const uint8_t*>(ob + off[14]);
+  a.V4mx = reinterpret_cast<const uint8_t*>(ob + off[15]);
+  a.fmt4 = fmt4;
   a.keys = reinterpret_cast<const uint16_t*>(lb + lo[0]);
   a.counts = reinterpret_cast<const int32_t*>(lb + lo[1]);
   a.order = reinterpret_cast<const int32_t*>(lb + lo[2]);

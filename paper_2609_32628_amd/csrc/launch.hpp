@@ -55,7 +55,9 @@ struct PrepArgs {
   uint8_t* V8;
   float *dQ, *dK, *dV, *g;
   _Float16 *Q16, *K16, *V16;  // 16-bit path operands (written when with16)
+  uint8_t *Q4mx, *K4mx, *V4mx;  // MXFP4 operands (written instead of Q4/K4/V4 when fmt4 = MXFP4)
   int with16;
+  int fmt4;
 };
 
 struct AttnArgs {
@@ -64,6 +66,8 @@ struct AttnArgs {
   const uint8_t* V8;
   const float *dQ, *dK, *dV, *g;
   const _Float16 *Q16, *K16, *V16;
+  const uint8_t *Q4mx, *K4mx, *V4mx;
+  int fmt4;
   const uint16_t* keys;
   const int32_t* counts;
   const int32_t* order;

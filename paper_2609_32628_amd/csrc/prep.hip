@@ -160,13 +160,30 @@ __device__ inline void nvfp4_group16(const float* x, float gX, float sixg, uint4
   hi = nvfp4_values8(y + 8, s2);
 }
 
+// ---- MXFP4 --------------------------------------------------------------------
+// E8M0 exponent of a 32-element block with largest magnitude amax >= 0:
+// floor(log2 amax) - 2, clamped below at -127 (zero and subnormal amax give
+// -127); finite fp32 amax keeps it below 126.
+__device__ inline int mx_exponent(float amax) { return max((int)(__float_as_uint(amax) >> 23) - 129, -127); }
+// 2^-k as a float (normal for every k from mx_exponent).
+__device__ inline float mx_inv_scale(int k) { return __uint_as_float(static_cast<uint32_t>(127 - k) << 23); }
+// E2M1 codes of 8 values, value e in nibble e (low nibble first).
+__device__ inline uint32_t fp4_codes8(const float* y) {
+  uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[2], y[3], 1.0f, 1);
+  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[4], y[5], 1.0f, 2);
+  return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[6], y[7], 1.0f, 3);
+}
+// MXFP4 sections: bytes per block (d/32 data fragments and the scale fragment).
+constexpr int mx_block_bytes(int D) { return 1024 * (D / 32 + 1); }
+
 // ---- Q and K ----------------------------------------------------------------
 template <int D, typename T>
 __global__ __launch_bounds__(256) void prep_qk_kernel(PrepArgs args) {
   constexpr int EPC = 16 / sizeof(T);
   constexpr int NG = D / 16;                // 16-channel groups per slot
   constexpr int UPT = kCap * NG / 256;      // groups per thread
-  constexpr int NS32 = D / 32;
+  constexpr int NS32 = D / 32, NS64 = D / 64;
   __shared__ float s_red[4];
   const int a = blockIdx.x, bh = blockIdx.y, which = blockIdx.z;  // which: 0 = Q, 1 = K
   const int b = bh / args.H, h = bh % args.H, R = args.R, tid = threadIdx.x;
@@ -214,11 +231,39 @@ __global__ __launch_bounds__(256) void prep_qk_kernel(PrepArgs args) {
     const int64_t c8 = ((int64_t)(jq * NS32 + (c16 >> 1)) * 64 + r + 32 * (c16 & 1)) * 16;
     *reinterpret_cast<uint4*>(out8 + c8) = int8_codes16(x[k], inv8);
     // NVFP4 chunks: [jq][c16][lane = r + 32 g][8] for halves g = 0, 1
-    uint4 lo, hi;
-    nvfp4_group16(x[k], gX, sixg, lo, hi);
     const int64_t c4 = ((int64_t)(jq * NG + c16) * 64 + r) * 8;
-    *reinterpret_cast<uint4*>(out4 + c4) = lo;
-    *reinterpret_cast<uint4*>(out4 + c4 + 32 * 8) = hi;
+    if (args.fmt4 == DA2_FMT4_NVFP4) {
+      uint4 lo, hi;
+      nvfp4_group16(x[k], gX, sixg, lo, hi);
+      *reinterpret_cast<uint4*>(out4 + c4) = lo;
+      *reinterpret_cast<uint4*>(out4 + c4 + 32 * 8) = hi;
+    } else {
+      // MXFP4: the 32-channel block is this group and its neighbour c16 ^ 1,
+      // held by the adjacent lane. The group's 16 codes are half of a lane's
+      // 16 bytes in data fragment (tile, s = c16/4), lane row + 32 ((c16/2)%2),
+      // where (tile, row) places the slot by kappa_mx for K.
+      float m16 = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) m16 = fmaxf(m16, fabsf(x[k][e]));
+      const int ke = mx_exponent(fmaxf(m16, __shfl_xor(m16, 1, 64)));
+      const float inv = mx_inv_scale(ke);
+      float y[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) y[e] = __fmul_rn(x[k][e], inv);  // exact (power of two)
+      const int slot = which == 0 ? rr : kappa(jq, r);
+      const int tile = which == 0 ? jq : (slot >> 4) & 1;
+      const int row = which == 0 ? r : 8 * ((slot & 15) >> 2) + 4 * (slot >> 5) + (slot & 3);
+      const int s = c16 >> 2, ml = row + 32 * ((c16 >> 1) & 1);
+      uint8_t* base = (which == 0 ? args.Q4mx : args.K4mx) + blk * (int64_t)mx_block_bytes(D);
+      *reinterpret_cast<uint2*>(base + ((tile * NS64 + s) * 64 + ml) * 16 + 8 * (c16 & 1)) =
+          make_uint2(fp4_codes8(y), fp4_codes8(y + 8));
+      if ((c16 & 1) == 0) {  // scale word tile*NS64+s of lane ml; unused words are zero
+        uint32_t* sw = reinterpret_cast<uint32_t*>(base + (2 * NS64 * 64 + ml) * 16);
+        sw[tile * NS64 + s] = static_cast<uint32_t>(ke + 127);
+        if (2 * NS64 < 4 && tile == 0 && s == 0)
+          for (int wd = 2 * NS64; wd < 4; ++wd) sw[wd] = 0u;
+      }
+    }
     if (args.with16) {  // 16-bit path: the same chunks as fp16(x)
       _Float16* out16 = (which == 0 ? args.Q16 : args.K16) + blk * (int64_t)kCap * D;
       *reinterpret_cast<uint4*>(out16 + c4) = half8(x[k]);
@@ -298,15 +343,49 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
       }
       *reinterpret_cast<uint4*>(args.V8 + blk * (int64_t)kCap * D + ((int64_t)(2 * t + (sg >> 1)) * 64 + lane) * 16) = code;
       // NVFP4 along slots: chunks [t][s = 2 (sg/2) + half][lane][8]
-      uint4 lo, hi;
-      nvfp4_group16(xc, gV, sixg, lo, hi);
       const int64_t c4 = blk * (int64_t)kCap * D + ((int64_t)(4 * t + 2 * (sg >> 1)) * 64 + lane) * 8;
-      *reinterpret_cast<uint4*>(args.V4 + c4) = lo;
-      *reinterpret_cast<uint4*>(args.V4 + c4 + 64 * 8) = hi;
+      if (args.fmt4 == DA2_FMT4_NVFP4) {
+        uint4 lo, hi;
+        nvfp4_group16(xc, gV, sixg, lo, hi);
+        *reinterpret_cast<uint4*>(args.V4 + c4) = lo;
+        *reinterpret_cast<uint4*>(args.V4 + c4 + 64 * 8) = hi;
+      }
       if (args.with16) {  // 16-bit path: the same chunks as fp16(v)
         *reinterpret_cast<uint4*>(args.V16 + c4) = half8(xc);
         *reinterpret_cast<uint4*>(args.V16 + c4 + 64 * 8) = half8(xc + 8);
       }
+    }
+  }
+  // MXFP4 along slots: unit = channel pair p, 32-slot block hb; the block's
+  // 32 codes fill the 16 bytes of lane c%32 + 32 hb in data fragment t = c/32.
+  constexpr int NT = D / 32;
+  if (args.fmt4 == DA2_FMT4_MXFP4 && tid < D) {
+    const int hb = tid / (D / 2);
+    float x0[32], x1[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const float2 f = tile_pair(tile, D, 32 * hb + i, p);
+      x0[i] = f.x;
+      x1[i] = f.y;
+    }
+    uint8_t* base = args.V4mx + blk * (int64_t)mx_block_bytes(D);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      float* xc = q == 0 ? x0 : x1;
+      const int c = 2 * p + q, t = c >> 5, ml = (c & 31) + 32 * hb;
+      float m = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) m = fmaxf(m, fabsf(xc[i]));
+      const int ke = mx_exponent(m);
+      const float inv = mx_inv_scale(ke);
+#pragma unroll
+      for (int i = 0; i < 32; ++i) xc[i] = __fmul_rn(xc[i], inv);  // exact (power of two)
+      *reinterpret_cast<uint4*>(base + (t * 64 + ml) * 16) =
+          make_uint4(fp4_codes8(xc), fp4_codes8(xc + 8), fp4_codes8(xc + 16), fp4_codes8(xc + 24));
+      uint32_t* sw = reinterpret_cast<uint32_t*>(base + (NT * 64 + ml) * 16);
+      sw[t] = static_cast<uint32_t>(ke + 127);
+      if (NT < 4 && t == 0)
+        for (int wd = NT; wd < 4; ++wd) sw[wd] = 0u;
     }
   }
   if (a == 0) {

@@ -33,6 +33,7 @@ class Workload:
     seed: int = 0
     num16: int = 0                  # num16/den of the pairs go to the 16-bit path
     partition: str = "tiles8"       # "tiles8" (8x8 tiles) or "ragged" (minimum-perimeter regions)
+    fmt4: str = "nvfp4"             # 4-bit encoding: "nvfp4" (the paper's) or "mxfp4"
 
     @property
     def N(self) -> int:

@@ -62,6 +62,64 @@ def index_v8(d):
     return np.broadcast_arrays(slot, ch)
 
 
+def kappa_mx(j, r):
+    return 32 * ((r // 4) % 2) + 16 * j + 4 * (r // 8) + r % 4
+
+
+def index_mx_qk(d, permute_keys):
+    """(slot, ch) index arrays [2, d/64, 64, 32] of the codes in the data
+    fragments of the Q4mx / K4mx sections (tile, step, lane, code)."""
+    r, g = _lanes()
+    jq = np.arange(2)[:, None, None, None]
+    s = np.arange(d // 64)[None, :, None, None]
+    i = np.arange(32)[None, None, None, :]
+    rr, gg = r[None, None, :, None], g[None, None, :, None]
+    slot = kappa_mx(jq, rr) if permute_keys else 32 * jq + rr
+    ch = 64 * s + 32 * gg + i
+    return np.broadcast_arrays(slot, ch)
+
+
+def index_mx_v(d):
+    """(slot, ch) index arrays [d/32, 64, 32] of the V4mx data codes."""
+    r, g = _lanes()
+    t = np.arange(d // 32)[:, None, None]
+    i = np.arange(32)[None, None, :]
+    rr, gg = r[None, :, None], g[None, :, None]
+    return np.broadcast_arrays(32 * gg + i, 32 * t + rr)
+
+
+def _pack_nibbles(codes):
+    """[..., 32] 4-bit codes -> [..., 16] bytes, code 2b in the low nibble of byte b."""
+    c = codes.astype(np.uint8)
+    return (c[..., 0::2] & 0xF) | ((c[..., 1::2] & 0xF) << 4)
+
+
+def mx_section(kind, codes, kexp):
+    """Bytes [R, (d/32 + 1) * 1024] of an MXFP4 section.
+
+    kind "Q", "K": codes [R, 64, d] (slot ordered), kexp [R, 64, d/32] block
+    exponents of (slot, 32-channel block); kind "V": codes [R, 64, d],
+    kexp [R, 2, d] of (32-slot block, channel)."""
+    R, _, d = codes.shape
+    r, g = _lanes()
+    words = np.zeros((R, 64, 4), np.uint32)
+    if kind in ("Q", "K"):
+        slot, ch = index_mx_qk(d, kind == "K")
+        data = codes[:, slot, ch]                                     # [R, 2, d/64, 64, 32]
+        data = data.reshape(R, 2 * (d // 64), 64, 32)
+        for jq in range(2):
+            for s in range(d // 64):
+                srow = kappa_mx(jq, r) if kind == "K" else 32 * jq + r
+                words[:, :, jq * (d // 64) + s] = kexp[:, srow, 2 * s + g] + 127
+    else:
+        slot, ch = index_mx_v(d)
+        data = codes[:, slot, ch]                                     # [R, d/32, 64, 32]
+        for t in range(d // 32):
+            words[:, :, t] = kexp[:, g, 32 * t + r] + 127
+    frags = np.concatenate([_pack_nibbles(data), words.view(np.uint8).reshape(R, 1, 64, 16)], axis=1)
+    return frags.reshape(R, -1)
+
+
 SECTIONS = {
     "Q4": (lambda d: index_q4(d, False), np.float16),
     "K4": (lambda d: index_q4(d, True), np.float16),

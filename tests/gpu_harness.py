@@ -10,7 +10,7 @@ import torch
 from oracle import encode, formats, partition, pipeline, rank
 from paper_2609_32628_amd import api
 from synth import configs, gen
-from fraglayout import to_frag
+from fraglayout import mx_section, to_frag
 
 TOL_MAX_ABS = 2e-2     # output tolerances of the parity bar
 TOL_REL_L2 = 5e-3
@@ -49,7 +49,9 @@ def sections(buf, p):
     specs = [("Q4", np.float16, (R, 64 * d)), ("K4", np.float16, (R, 64 * d)), ("V4", np.float16, (R, 64 * d)),
              ("Q8", np.int8, (R, 64 * d)), ("K8", np.int8, (R, 64 * d)), ("V8", np.uint8, (R, 64 * d)),
              ("dQ", np.float32, (R,)), ("dK", np.float32, (R,)), ("dV", np.float32, (d,)), ("g", np.float32, (4,)),
-             ("Q16", np.float16, (R, 64 * d)), ("K16", np.float16, (R, 64 * d)), ("V16", np.float16, (R, 64 * d))]
+             ("Q16", np.float16, (R, 64 * d)), ("K16", np.float16, (R, 64 * d)), ("V16", np.float16, (R, 64 * d)),
+             ("Q4mx", np.uint8, (R, (d // 32 + 1) * 1024)), ("K4mx", np.uint8, (R, (d // 32 + 1) * 1024)),
+             ("V4mx", np.uint8, (R, (d // 32 + 1) * 1024))]
     for i, (name, dt, shape) in enumerate(specs):
         nbytes = BH * int(np.prod(shape)) * np.dtype(dt).itemsize
         out[name] = raw[off[i]:off[i] + nbytes].view(dt).reshape((BH,) + shape)
@@ -85,12 +87,21 @@ def write_lists(buf, p, cls_all):
     buf.lists.copy_(torch.from_numpy(raw))
 
 
-def expected_sections(enc):
-    """Oracle encodings of one head in the ops-buffer order."""
+def expected_mx_sections(enc_mx):
+    """Oracle MXFP4 encodings of one head as the bytes of sections 13..15."""
+    return {name + "4mx": mx_section(name, formats.e2m1_code(enc_mx["e" + name]), enc_mx["k" + name])
+            for name in ("Q", "K", "V")}
+
+
+def expected_sections(enc, enc_mx=None):
+    """Oracle encodings of one head in the ops-buffer order (the MXFP4
+    sections only when ``enc_mx`` is given)."""
     sQ = np.repeat(enc["sQ"], 16, axis=2) * enc["eQ"]
     sK = np.repeat(enc["sK"], 16, axis=2) * enc["eK"]
     sV = np.repeat(enc["sV"], 16, axis=1) * enc["eV"]
+    mx = {} if enc_mx is None else expected_mx_sections(enc_mx)
     return {
+        **mx,
         "Q4": to_frag("Q4", sQ), "K4": to_frag("K4", sK), "V4": to_frag("V4", sV),
         "Q8": to_frag("Q8", enc["q8"]), "K8": to_frag("K8", enc["k8"]),
         "V8": to_frag("V8", formats.e4m3_code(enc["v8"])),
@@ -101,13 +112,17 @@ def expected_sections(enc):
     }
 
 
-def write_ops(buf, p, encs):
-    """Oracle encodings of every head -> the ops buffer (stage injection)."""
+def write_ops(buf, p, encs, encs_mx=None):
+    """Oracle encodings of every head -> the ops buffer (stage injection);
+    the MXFP4 sections too when ``encs_mx`` is given."""
     off = api.da2_ops_offsets(p)
     raw = buf.ops.cpu().numpy()
     order = ["Q4", "K4", "V4", "Q8", "K8", "V8", "dQ", "dK", "dV", "g", "Q16", "K16", "V16"]
+    if encs_mx is not None:
+        order += ["Q4mx", "K4mx", "V4mx"]
+    exp = [expected_sections(e, None if encs_mx is None else encs_mx[i]) for i, e in enumerate(encs)]
     for i, name in enumerate(order):
-        arr = np.stack([expected_sections(e)[name] for e in encs])
+        arr = np.stack([x[name] for x in exp])
         b = np.ascontiguousarray(arr).view(np.uint8).reshape(-1)
         raw[off[i]:off[i] + b.size] = b
     buf.ops.copy_(torch.from_numpy(raw))

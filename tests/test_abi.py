@@ -54,7 +54,9 @@ def test_sizes_mid_layer():
     assert off == sorted(off) and all(o % 256 == 0 for o in off)
     e = 12 * 37632 * 128
     assert off[1] - off[0] >= 2 * e and off[4] - off[3] >= e
-    assert s["ops_bytes"] >= off[12] + 2 * e and len(off) == 13
+    mx = 12 * 588 * 5 * 1024   # MXFP4 sections: d/32 + 1 fragments of 1 KB per block
+    assert off[13] - off[12] >= 2 * e and off[14] - off[13] >= mx and off[15] - off[14] >= mx
+    assert s["ops_bytes"] >= off[15] + mx and len(off) == 16
     lo = api.da2_lists_offsets(_p(configs.MID))
     assert lo[1] >= 2 * 12 * 588 * 588 and lo[2] - lo[1] >= 16 * 12 * 588 and s["lists_bytes"] >= lo[3] + 32
     wo = api.da2_ws_draft_offsets(_p(configs.MID))
@@ -136,11 +138,15 @@ def test_compute_calls_validate_before_gpu():
     assert L.da2_rank_assign(FAKE, p, 0, 10, 30, 100, 0, FAKE, FAKE, FAKE, wr - 1, None) == W
     big = api.problem(1, 1, 128, 33, 128, 128)           # R^2 >= 2^22 in head scope
     assert L.da2_rank_assign(FAKE, big, 0, 10, 30, 100, 0, FAKE, FAKE, FAKE, 1 << 40, None) == E
-    assert L.da2_prep_operands(FAKE, None, FAKE, d, FAKE, p, 0, FAKE, FAKE, None, 0, None) == E
-    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(dtype=3), FAKE, p, 0, FAKE, FAKE, None, 0, None) == E
-    assert L.da2_prep_operands(FAKE, FAKE, FAKE, d, FAKE, p, 2, FAKE, FAKE, None, 0, None) == E
-    assert L.da2_mixed_attn(FAKE, FAKE, None, p, d, FAKE, None) == E
-    assert L.da2_mixed_attn(FAKE, FAKE, FAKE, p, _desc(dtype=9), FAKE, None) == E
+    assert L.da2_prep_operands(FAKE, None, FAKE, d, FAKE, p, 0, 0, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(dtype=3), FAKE, p, 0, 0, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, d, FAKE, p, 2, 0, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, d, FAKE, p, 0, 2, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, d, FAKE, p, 0, -1, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_mixed_attn(FAKE, FAKE, None, p, 0, d, FAKE, None) == E
+    assert L.da2_mixed_attn(FAKE, FAKE, FAKE, p, 0, _desc(dtype=9), FAKE, None) == E
+    assert L.da2_mixed_attn(FAKE, FAKE, FAKE, p, 2, d, FAKE, None) == E
+    assert L.da2_mixed_attn(FAKE, FAKE, FAKE, p, -1, d, FAKE, None) == E
 
 
 def test_inputs_must_allow_16_byte_loads():
@@ -154,9 +160,9 @@ def test_inputs_must_allow_16_byte_loads():
     ws = s["ws_draft_bytes"]
     assert L.da2_draft_map(odd, FAKE, _desc(), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
     assert L.da2_draft_map(FAKE, odd, _desc(), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
-    assert L.da2_prep_operands(FAKE, FAKE, odd, _desc(), FAKE, p, 0, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, odd, _desc(), FAKE, p, 0, 0, FAKE, FAKE, None, 0, None) == E
     assert L.da2_draft_map(FAKE, FAKE, _desc(sn=132), FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
-    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(sn=130), FAKE, p, 0, FAKE, FAKE, None, 0, None) == E
+    assert L.da2_prep_operands(FAKE, FAKE, FAKE, _desc(sn=130), FAKE, p, 0, 0, FAKE, FAKE, None, 0, None) == E
     f32 = _lib.Tensor(12 * 32760 * 128 + 2, 32760 * 128, 128, _lib.DA2_FP32, 0)
     assert L.da2_draft_map(FAKE, FAKE, f32, FAKE, p, 0.2, FAKE, FAKE, FAKE, ws, None) == E
     # fp32 rows need only 4-element alignment: the stride check passes and the

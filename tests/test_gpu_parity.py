@@ -46,7 +46,7 @@ def _run_gpu(w, Q, K, V, budgets=None, scope=None, odtype=torch.float32):
     buf = api.alloc(p, scope)
     Qd, Kd, Vd = (to_device(X, w) for X in (Q, K, V))
     O = torch.full(Qd.shape, float("nan"), dtype=odtype, device="cuda")
-    api.attention(Qd, Kd, Vd, buf, w.lam, budgets, O, num16=w.num16)
+    api.attention(Qd, Kd, Vd, buf, w.lam, budgets, O, num16=w.num16, fmt4=w.fmt4)
     torch.cuda.synchronize()
     return buf, p, O
 
@@ -129,7 +129,7 @@ def test_prep_operands(w):
     buf = api.alloc(p, w.scope)
     Qd, Kd, Vd = (to_device(X, w) for X in (Q, K, V))
     api.da2_draft_map(Qd, Kd, buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
-    api.da2_prep_operands(Qd, Kd, Vd, buf.layout, p, 1, buf.stats, buf.ops, None)
+    api.da2_prep_operands(Qd, Kd, Vd, buf.layout, p, 1, "nvfp4", buf.stats, buf.ops, None)
     torch.cuda.synchronize()
     got = sections(buf, p)
     slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
@@ -141,6 +141,32 @@ def test_prep_operands(w):
             gv, wv = got[name][bh].view(np.uint16), want[name].view(np.uint16)
             assert np.array_equal(gv, wv), (name, bh, int((gv != wv).sum()))
         for name in ("Q8", "K8", "V8"):
+            assert np.array_equal(got[name][bh], want[name]), (name, bh, int((got[name][bh] != want[name]).sum()))
+        for name in ("dQ", "dK", "dV", "g"):
+            assert np.array_equal(got[name][bh].view(np.uint32), want[name].view(np.uint32)), (name, bh)
+
+
+@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED], ids=lambda w: w.name)
+def test_prep_operands_mxfp4(w):
+    """fmt4 = MXFP4: the three MXFP4 sections byte for byte (codes, scale
+    words, unused words zero), and the 8-bit sections unchanged."""
+    log(f"prep_operands mxfp4 parity {w.name}")
+    Q, K, V = inputs(w)
+    p = problem_of(w)
+    buf = api.alloc(p, w.scope)
+    buf.ops.fill_(0xA5)     # the MXFP4 sections must be fully written
+    Qd, Kd, Vd = (to_device(X, w) for X in (Q, K, V))
+    api.da2_draft_map(Qd, Kd, buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
+    api.da2_prep_operands(Qd, Kd, Vd, buf.layout, p, 0, "mxfp4", buf.stats, buf.ops, None)
+    torch.cuda.synchronize()
+    got = sections(buf, p)
+    slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
+    for bh in range(w.B * w.H):
+        b, h = divmod(bh, w.H)
+        enc = oenc.encode_head(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
+        enc_mx = oenc.encode_head_mx(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
+        want = expected_sections(enc, enc_mx)
+        for name in ("Q4mx", "K4mx", "V4mx", "Q8", "K8", "V8"):
             assert np.array_equal(got[name][bh], want[name]), (name, bh, int((got[name][bh] != want[name]).sum()))
         for name in ("dQ", "dK", "dV", "g"):
             assert np.array_equal(got[name][bh].view(np.uint32), want[name].view(np.uint32)), (name, bh)
@@ -185,8 +211,39 @@ def test_mixed_attn_injected(w, budgets16):
     compare_outputs(Og, ref, f"{w.name} {num16} {budgets}")
 
 
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+@pytest.mark.parametrize("budgets16", [None, (0, 0, 40, 100), (0, 5, 45, 100), (15, 10, 30, 100)])
+def test_mixed_attn_injected_mxfp4(w, budgets16):
+    """fmt4 = MXFP4: oracle MXFP4 operands and lists in, the 4-bit phase on
+    scaled fp4 MFMAs, oracle attention (MXFP4 weights) to compare."""
+    num16, budgets = (0, w.budgets) if budgets16 is None else (budgets16[0], budgets16[1:])
+    log(f"mixed_attn mxfp4 stage parity {w.name} {num16} {budgets}")
+    Q, K, V = inputs(w)
+    p = problem_of(w)
+    buf = api.alloc(p, w.scope)
+    encs, clss, (slot2tok, n_a) = _oracle_encs_cls(w, Q, K, V, budgets, w.scope, num16)
+    encs_mx = [oenc.encode_head_mx(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
+               for b in range(w.B) for h in range(w.H)]
+    write_ops(buf, p, encs, encs_mx)
+    write_lists(buf, p, clss)
+    O = torch.full((w.B, w.H, w.N, w.d), float("nan"), dtype=torch.float32, device="cuda")
+    api.da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, fmt4="mxfp4")
+    torch.cuda.synchronize()
+    Og = O.cpu().numpy().reshape(-1, w.N, w.d)
+    assert not np.isnan(Og).any()
+    ref = np.empty_like(Og, dtype=np.float64)
+    for bh, (enc, enc_mx, cls) in enumerate(zip(encs, encs_mx, clss)):
+        ops = oatt.Operands.quantized(oenc.reconstruct(enc), n_a, oenc.reconstruct_mx(enc_mx))
+        for a in range(n_a.size):
+            ref[bh, slot2tok[a * 64:a * 64 + n_a[a]]] = oatt.attend(ops, a, *orank.key_lists_all(cls[a]))
+    compare_outputs(Og, ref, f"{w.name} mxfp4 {num16} {budgets}")
+
+
 E2E_CASES = CASES + [replace(SMALL, name="small-16bit-15/10/30", num16=15), SMALL_RAGGED,
-                     replace(SMALL_RAGGED, name="small-ragged-16bit", num16=20, scope="row")]
+                     replace(SMALL_RAGGED, name="small-ragged-16bit", num16=20, scope="row"),
+                     replace(configs.TINY, name="tiny-mxfp4", fmt4="mxfp4"),
+                     replace(SMALL, name="small-mxfp4", fmt4="mxfp4"),
+                     replace(SMALL_RAGGED, name="small-ragged-mxfp4-16bit", fmt4="mxfp4", num16=10)]
 
 
 @pytest.mark.parametrize("w", E2E_CASES, ids=lambda w: w.name)
@@ -259,6 +316,30 @@ def test_mid_layer_ragged_sampled_rows():
     for a in np.nonzero((cls_g != o["cls"]).any(axis=1))[0]:
         ref[slot2tok[a * 64:a * 64 + n_a[a]]] = np.nan
     compare_outputs(O.cpu().numpy()[0, 0], ref, f"mid ragged (head 3 inputs), near-tie mismatches {n_bad}")
+
+
+def test_mid_layer_mxfp4_sampled_rows():
+    """The mid layer with the MXFP4 4-bit path, in the launch configuration
+    the benchmark times with --fmt4 mxfp4 (all 12 heads on the GPU); the
+    oracle checks two heads on a seeded sample of query blocks."""
+    w = replace(configs.MID, fmt4="mxfp4")
+    log("end-to-end parity mid layer, mxfp4, sampled rows")
+    Q, K, V = inputs(w)
+    buf, p, O = _run_gpu(w, Q, K, V)
+    R = buf.sizes["R"]
+    rows = sorted(np.random.default_rng(2).choice(R, 16, replace=False))
+    Og = O.cpu().numpy()
+    cls_g = buf.cls.cpu().numpy()
+    T8, T4 = orank.quotas(*w.budgets, R * R)
+    for h in (2, 9):
+        layout, outs = pipeline.run(w, Q[:, h:h + 1], K[:, h:h + 1], V[:, h:h + 1], rows=rows)
+        o = outs[0]
+        n_bad = mask_mismatches(cls_g[0, h], o["cls"], o["A32"], (0, T8, T4), "head")
+        ref = o["O"].copy()
+        slot2tok, n_a, _ = layout
+        for a in np.nonzero((cls_g[0, h] != o["cls"]).any(axis=1))[0]:
+            ref[slot2tok[a * 64:a * 64 + n_a[a]]] = np.nan
+        compare_outputs(Og[0, h], ref, f"mid mxfp4 head {h}, near-tie mismatches {n_bad}")
 
 
 def test_bf16_output_and_determinism():
