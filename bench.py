@@ -70,6 +70,124 @@ def recorded_traffic(workload):
     return rec.get("read_bytes", 0) + rec.get("write_bytes", 0)
 
 
+# ---- operator error-vs-latency sweep (attention error analysis) -------------
+# Precision mixes as percentages of the retained pairs on the (16, 8, 4)-bit
+# paths, and the retained fractions swept at each mix (1.0 = no sparsity).
+SWEEP_MIXES = {"4": (0, 0, 100), "8": (0, 100, 0), "16": (100, 0, 0),
+               "8/16": (10, 90, 0), "4/8": (0, 25, 75), "4/8/16": (10, 30, 60)}
+SWEEP_RETAINED = (0.05, 0.1, 0.2, 0.3, 0.5, 0.7, 1.0)
+SWEEP_DEN = 1000
+
+
+def sweep_points():
+    """(lambda, mix, retained, fmt4) of every sweep point: all mixes with the
+    max-pooled draft (lambda = 0.2), the 8-bit and 8/16 mixes also with average
+    pooling alone (lambda = 0), and the mixes with a 4-bit share also with MXFP4."""
+    pts = [(0.2, m, r, "nvfp4") for m in SWEEP_MIXES for r in SWEEP_RETAINED]
+    pts += [(0.0, m, r, "nvfp4") for m in ("8", "8/16") for r in SWEEP_RETAINED]
+    pts += [(0.2, m, r, "mxfp4") for m in ("4", "4/8", "4/8/16") for r in SWEEP_RETAINED]
+    return pts
+
+
+def sweep_budgets(mix, retained):
+    """(num16, num8, num4) out of SWEEP_DEN for a mix at a retained fraction."""
+    return tuple(int(retained * pct * SWEEP_DEN / 100 + 0.5) for pct in SWEEP_MIXES[mix])
+
+
+def _sweep_head(h):
+    from synth import configs, gen
+    Q, K, V = gen.generate(configs.FIG4, heads=[h])
+    return Q[0, 0], K[0, 0], V[0, 0]
+
+
+def dense_rows(q, K, V):
+    """Textbook softmax(q K^T / sqrt d) V in float64 for a few query rows: the
+    dense output the error metric compares against."""
+    S = q.astype(np.float64) @ K.astype(np.float64).T / np.sqrt(K.shape[1])
+    P = np.exp(S - S.max(axis=1, keepdims=True))
+    return (P / P.sum(axis=1, keepdims=True)) @ V.astype(np.float64)
+
+
+def run_sweep(args):
+    """Relative L2 error against dense attention versus the latency of the whole
+    operator (draft map, ranking, operand preparation, attention), one JSON line
+    per point. Latency: median of three timed steps after one warm-up. Error:
+    over a seeded sample of query rows (8 heads x 64 tokens) whose dense output
+    is computed in float64 on the host."""
+    from multiprocessing import get_context
+
+    from synth import configs
+    w = configs.FIG4
+    # inputs drawn head by head in worker processes, before the GPU is touched
+    workers = min(16, os.cpu_count() or 1)
+    heads = []
+    with get_context("fork").Pool(workers) as pool:
+        for i, hv in enumerate(pool.imap(_sweep_head, range(w.H))):
+            heads.append(hv)
+            if (i + 1) % 8 == 0:
+                print(f"sweep inputs: {i + 1}/{w.H} heads", file=sys.stderr, flush=True)
+    rng = np.random.default_rng(7)
+    ref_heads = sorted(rng.choice(w.H, 8, replace=False))
+    ref_rows = {h: np.sort(rng.choice(w.N, 64, replace=False)) for h in ref_heads}
+    ref = {h: dense_rows(heads[h][0][ref_rows[h]], heads[h][1], heads[h][2]) for h in ref_heads}
+    print("sweep dense reference rows ready", file=sys.stderr, flush=True)
+
+    import torch
+
+    from paper_2609_32628_amd import api
+    dev = []
+    for t in range(3):
+        X = torch.empty((1, w.H, w.N, w.d), dtype=torch.bfloat16, device="cuda")
+        for h in range(w.H):
+            X[0, h].copy_(torch.from_numpy(heads[h][t]).to(torch.bfloat16))
+        dev.append(X)
+    del heads
+    p = api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg, w.partition)
+    buf = api.alloc(p, "head")
+    O = torch.empty(dev[0].shape, dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+    idx_h = torch.tensor(ref_heads, device="cuda")
+    for lam, mix, rho, fmt4 in sweep_points():
+        n16, n8, n4 = sweep_budgets(mix, rho)
+
+        def step(ev=None):
+            api.da2_draft_map(dev[0], dev[1], buf.layout, p, lam, buf.A, buf.stats, buf.ws_draft)
+            api.da2_rank_assign(buf.A, p, n16, n8, n4, SWEEP_DEN, "head", buf.cls, buf.lists, buf.ws_rank)
+            api.da2_prep_operands(dev[0], dev[1], dev[2], buf.layout, p, int(n16 > 0), fmt4, buf.stats, buf.ops,
+                                  None)
+            if ev is not None:
+                ev[0].record(stream)
+            api.da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, fmt4=fmt4)
+            if ev is not None:
+                ev[1].record(stream)
+
+        step()
+        torch.cuda.synchronize()
+        total, attn = [], []
+        for _ in range(3):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e[0].record(stream)
+            step(e[2:])
+            e[1].record(stream)
+            torch.cuda.synchronize()
+            total.append(e[0].elapsed_time(e[1]))
+            attn.append(e[2].elapsed_time(e[3]))
+        Os = O[0].index_select(0, idx_h).float().cpu().numpy()
+        num = den = 0.0
+        for i, h in enumerate(ref_heads):
+            diff = Os[i][ref_rows[h]].astype(np.float64) - ref[h]
+            num += float((diff ** 2).sum())
+            den += float((ref[h] ** 2).sum())
+        cls = buf.cls
+        rec = {"sweep": "operator error vs latency", "workload": w.name, "lambda": lam, "mix_16_8_4_pct": mix,
+               "retained": rho, "fmt4": fmt4, "budgets_16_8_4_of_1000": [n16, n8, n4],
+               "ms_median": float(np.median(total)), "mixed_attn_ms_median": float(np.median(attn)),
+               "rel_l2_pct": 100.0 * float(np.sqrt(num / den)),
+               "tiles": {str(c): int((cls == c).sum().item()) for c in (16, 8, 4)},
+               "error_sample": f"{len(ref_heads)} heads x 64 query tokens"}
+        print(json.dumps(rec), flush=True)
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -82,6 +200,9 @@ def parse():
                     help="num16/den of the region pairs on the 16-bit path (the hot path uses 0)")
     ap.add_argument("--fmt4", choices=("nvfp4", "mxfp4"), default="nvfp4",
                     help="encoding of the 4-bit path: the paper's NVFP4 (default) or gfx950's native MXFP4")
+    ap.add_argument("--sweep", action="store_true",
+                    help="operator error-vs-latency sweep over sparsity, precision mixes and lambda on the "
+                         "109,368-token x 56-head shape (one JSON line per point) instead of the benchmark")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 512 MiB device copy (HBM counter calibration)")
@@ -124,6 +245,9 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
               "the path shards by head with no exchange, so multi-GPU numbers are not produced.", file=sys.stderr)
         sys.exit(2)
+    if args.sweep:
+        run_sweep(args)
+        return
     import torch
 
     from paper_2609_32628_amd import api

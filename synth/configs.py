@@ -68,5 +68,13 @@ LONG = Workload("long-33x45x80-h24-d128", B=1, H=24, d=128, T=33, Hg=45, Wg=80,
                 dtype="bf16", budgets=(5, 25, 100), scope="head",
                 head_scale=True, phase_drift=True, seed=5)
 
-ALL = (TINY, MID) + SWEEP + (WIDE, LONG)
+# Operator error-vs-latency sweep shape (the paper's attention error analysis
+# uses a 109,376-token, 56-head, d=128 capture, which is not a product of a
+# latent grid; 31x42x84 = 109,368 tokens stands in for it), on the ragged
+# partition; budgets are set per sweep point.
+FIG4 = Workload("fig4-31x42x84-h56-d128", B=1, H=56, d=128, T=31, Hg=42, Wg=84,
+                dtype="bf16", budgets=(100, 0, 100), scope="head",
+                head_scale=True, seed=6, partition="ragged")
+
+ALL = (TINY, MID) + SWEEP + (WIDE, LONG, FIG4)
 BY_NAME = {w.name: w for w in ALL}
