@@ -316,7 +316,7 @@ __device__ inline void after(const T& v) {
 // first(S): logits of the first block. region1<MASK>(S, S', nb, dk): the
 // logit MFMAs of block i+1 interleaved with the first part of the softmax of
 // block i (MASK: block i is partial); region2(S): the rest of the softmax, after
-// sK has been handed to the next copy. pv(): the value product.
+// sK has been handed to the next copy. pv(S): the value product of block i.
 template <int NFK, typename Frag, typename SA, typename FIRST, typename STEP1, typename STEP2, typename PV>
 __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_a, const float* dKh,
                                   const Frag* Kh, const Frag* Vh, Frag* sK, Frag* sV, int wave, int lane,
@@ -379,7 +379,7 @@ __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_
     else
       wait_vmem_keep<0>();
     wg_barrier();
-    pv();
+    pv(Sc);
     wait_lds();
     wg_barrier();  // both waves are done with sV
     if (more1) dma_tile(Vh + (int64_t)kb1 * TILE, sV);
@@ -444,12 +444,12 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
     float gm0 = 0.0f, gm1 = 0.0f, mn = 0.0f;
     Fp4Group G0, G1;
     // Region 1: logits of the next block (NS16 stages of two MFMAs, operands
-    // read one stage ahead) with the row maxima and the first group's
-    // exponentials of the current block in five pieces over the stages.
+    // read one stage ahead) with the row maxima, the first group's weights and
+    // operands, and the second group's scale, in six pieces over the stages.
     auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float) {
       if constexpr (MASK) mask_tail(Sc, nb, g);
       f16x8 k0 = sK[lane], k1 = sK[NS16 * 64 + lane];
-      constexpr int NP = 5;
+      constexpr int NP = 6;
 #pragma unroll
       for (int s = 0; s < NS16; ++s) {
         f16x8 n0 = k0, n1 = k1;
@@ -472,8 +472,11 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
             fp4_exps<0, 5>(G0, Sc[0], c4);
           } else if (piece == 3) {
             fp4_exps<5, 10>(G0, Sc[0], c4);
-          } else {
+          } else if (piece == 4) {
             fp4_exps<10, 16>(G0, Sc[0], c4);
+          } else {
+            fp4_pack(G0, P[0], P[1]);
+            fp4_setup(G1, gm1, c4, mn);
           }
         }
         fence();
@@ -481,17 +484,13 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
         k1 = n1;
       }
     };
-    // Region 2: the second group's weights and both groups' fp16 operands.
-    auto region2 = [&](SA& Sc) {
-      fp4_pack(G0, P[0], P[1]);
-      fp4_setup(G1, gm1, c4, mn);
-      fp4_exps<0, 16>(G1, Sc[1], c4);
-      fp4_pack(G1, P[2], P[3]);
-      l += weight_sum(G0) + weight_sum(G1);
-      after(P[0]), after(P[1]), after(P[2]), after(P[3]), after(l);
-    };
-    // U += V^T P^T; value fragments are read two MFMAs ahead.
-    auto pv = [&]() {
+    // No separate region 2: the second group's weights are computed inside the
+    // value product, beside the MFMAs that use the first group's operands.
+    auto region2 = [&](SA&) {};
+    // U += V^T P^T; value fragments are read two MFMAs ahead. The MFMAs of the
+    // first group (k < 2 NT) carry the second group's exponentials and its
+    // fp16 operands, which the remaining MFMAs use.
+    auto pv = [&](SA& Sc) {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
       constexpr int NM = 4 * NT;
       auto vfrag = [&](int k) { return sV[((k % NT) * 4 + k / NT) * 64 + lane]; };
@@ -506,6 +505,16 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
             v0 = vfrag(k + 2);
         }
         U[k % NT] = __builtin_amdgcn_mfma_f32_32x32x16_f16(cur, P[k / NT], U[k % NT], 0, 0, 0);
+        // pieces of the second group, spread over the first group's MFMAs
+        constexpr int NG = 2 * NT;  // MFMAs that read P[0], P[1]
+        if (k == 0) fp4_exps<0, 4>(G1, Sc[1], c4);
+        if (k == NG / 4) fp4_exps<4, 8>(G1, Sc[1], c4);
+        if (k == NG / 2) fp4_exps<8, 12>(G1, Sc[1], c4);
+        if (k == 3 * NG / 4) fp4_exps<12, 16>(G1, Sc[1], c4);
+        if (k == NG - 1) {
+          fp4_pack(G1, P[2], P[3]);
+          l += weight_sum(G0) + weight_sum(G1);
+        }
         fence();
       }
     };
@@ -594,7 +603,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
       after(P), after(l), after(psc);
     };
     // U += V^T P^T: one scaled MFMA per channel tile.
-    auto pv = [&]() {
+    auto pv = [&](SA& Sc) {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
       const i32x4 vsw = sVm[NT * 64 + lane];
 #pragma unroll
@@ -689,7 +698,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
       after(P), after(l);
     };
     // U += V^T P^T (fp8 x fp8, unit scales); value fragments read one MFMA ahead.
-    auto pv = [&]() {
+    auto pv = [&](SA& Sc) {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
       auto vfrag = [&](int t) {
         const i32x4 v0 = sV8[(t * 2 + 0) * 64 + lane], v1 = sV8[(t * 2 + 1) * 64 + lane];
@@ -787,7 +796,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
       after(P[0]), after(P[1]), after(P[2]), after(P[3]), after(l);
     };
     // U += V^T P^T; value fragments are read two MFMAs ahead.
-    auto pv = [&]() {
+    auto pv = [&](SA& Sc) {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
       constexpr int NM = 4 * NT;
       auto vfrag = [&](int k) { return sV[((k % NT) * 4 + k / NT) * 64 + lane]; };
