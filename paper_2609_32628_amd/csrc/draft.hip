@@ -100,10 +100,14 @@ typedef double f64x4 __attribute__((ext_vector_type(4)));
 // float64 matrix cores: each wave owns a 32x32 quarter as 2x2 MFMA tiles of
 // 16x16x4. The reduction over channels may visit them in any order as long as
 // both operands agree: lane group q = lane/16 of k-step 2t+h reads channel
-// 8t + 2q + h, so one 16-byte load per operand tile feeds two k-steps. Rows
-// and columns beyond R read row R-1 and are not stored.
+// 8t + 2q + h, so one 16-byte load per operand tile feeds two k-steps. The
+// loads run one group of 8 channels ahead of the MFMAs, and the four
+// accumulators are updated in turn so that consecutive MFMAs are independent.
+// Rows and columns beyond R read row R-1 and are not stored.
+template <int D>
 __global__ __launch_bounds__(256) void draft_logits_kernel(DraftArgs args) {
-  const int R = args.R, d = args.d, bh = blockIdx.z >> 1, br = blockIdx.z & 1;
+  constexpr int d = D;
+  const int R = args.R, bh = blockIdx.z >> 1, br = blockIdx.z & 1;
   const double* Qs = (br == 0 ? args.Qbar : args.Qmax) + (int64_t)bh * R * d;
   const double* Ks = (br == 0 ? args.Kbar : args.Kmax) + (int64_t)bh * R * d;
   double* out = (br == 0 ? args.S1 : args.S2) + (int64_t)bh * R * R;
@@ -121,20 +125,32 @@ __global__ __launch_bounds__(256) void draft_logits_kernel(DraftArgs args) {
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
-  for (int t = 0; t < d; t += 8) {
-    double2 a[2], b[2];
+  double2 a[2][2], b[2][2];  // [buffer][tile]
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      a[i] = *reinterpret_cast<const double2*>(pa[i] + t);
-      b[i] = *reinterpret_cast<const double2*>(pb[i] + t);
+  for (int i = 0; i < 2; ++i) {
+    a[0][i] = *reinterpret_cast<const double2*>(pa[i]);
+    b[0][i] = *reinterpret_cast<const double2*>(pb[i]);
+  }
+#pragma unroll
+  for (int t = 0; t < d / 8; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < d / 8) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        a[cur ^ 1][i] = *reinterpret_cast<const double2*>(pa[i] + 8 * (t + 1));
+        b[cur ^ 1][i] = *reinterpret_cast<const double2*>(pb[i] + 8 * (t + 1));
+      }
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i].x, b[j].x, acc[i][j], 0, 0, 0);
-        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i].y, b[j].y, acc[i][j], 0, 0, 0);
-      }
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[cur][i].x, b[cur][j].x, acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[cur][i].y, b[cur][j].y, acc[i][j], 0, 0, 0);
   }
   // accumulator element e of lane l: row l/16 + 4e, column l%16
   const double sqd = sqrt((double)d);
@@ -155,7 +171,48 @@ __device__ inline double wave_max_f64(double v) {
 }
 
 // One wave per row of A (four rows per workgroup): the two row softmaxes (max
-// subtracted) mixed with weight lambda, rounded once to float32.
+// subtracted) mixed with weight lambda, rounded once to float32. Rows of up to
+// 64 KMAX entries keep their logits and exponentials in registers (one exp per
+// entry and branch); longer rows take the three-pass form below.
+template <int KMAX>
+__global__ __launch_bounds__(256) void draft_softmax_reg_kernel(DraftArgs args) {
+  const int R = args.R, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= (int64_t)args.B * args.H * R) return;
+  const double* s1 = args.S1 + row * R;
+  const double* s2 = args.S2 + row * R;
+  double e1[KMAX], e2[KMAX];
+  double m1 = -INFINITY, m2 = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    const int i = lane + 64 * k;
+    e1[k] = i < R ? s1[i] : -INFINITY;
+    e2[k] = i < R ? s2[i] : -INFINITY;
+    m1 = fmax(m1, e1[k]);
+    m2 = fmax(m2, e2[k]);
+  }
+  m1 = wave_max_f64(m1);
+  m2 = wave_max_f64(m2);
+  double z1 = 0.0, z2 = 0.0;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    const bool in = lane + 64 * k < R;
+    e1[k] = in ? exp(e1[k] - m1) : 0.0;
+    e2[k] = in ? exp(e2[k] - m2) : 0.0;
+    z1 += e1[k];
+    z2 += e2[k];
+  }
+  z1 = wave_sum_f64(z1);
+  z2 = wave_sum_f64(z2);
+  const double lam = args.lambda;
+  float* out = args.A + row * R;
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    const int i = lane + 64 * k;
+    if (i < R) out[i] = (float)((1.0 - lam) * (e1[k] / z1) + lam * (e2[k] / z2));
+  }
+}
+
 __global__ __launch_bounds__(256) void draft_softmax_kernel(DraftArgs args) {
   const int R = args.R, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -201,9 +258,18 @@ hipError_t launch_draft(const DraftArgs& args, hipStream_t stream) {
       hipLaunchKernelGGL((draft_pool_kernel<64, float>), pool_grid, dim3(256), 0, stream, args);
   }
   const int nt = (args.R + 63) / 64;
-  hipLaunchKernelGGL(draft_logits_kernel, dim3(nt, nt, 2 * BH), dim3(256), 0, stream, args);
+  if (args.d == 128)
+    hipLaunchKernelGGL(draft_logits_kernel<128>, dim3(nt, nt, 2 * BH), dim3(256), 0, stream, args);
+  else
+    hipLaunchKernelGGL(draft_logits_kernel<64>, dim3(nt, nt, 2 * BH), dim3(256), 0, stream, args);
   const int64_t rows = (int64_t)BH * args.R;
-  hipLaunchKernelGGL(draft_softmax_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, args);
+  const dim3 sgrid((unsigned)((rows + 3) / 4));
+  if (args.R <= 64 * 10)
+    hipLaunchKernelGGL(draft_softmax_reg_kernel<10>, sgrid, dim3(256), 0, stream, args);
+  else if (args.R <= 64 * 32)
+    hipLaunchKernelGGL(draft_softmax_reg_kernel<32>, sgrid, dim3(256), 0, stream, args);
+  else
+    hipLaunchKernelGGL(draft_softmax_kernel, sgrid, dim3(256), 0, stream, args);
   return hipGetLastError();
 }
 
