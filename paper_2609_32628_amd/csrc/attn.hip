@@ -237,24 +237,29 @@ __device__ inline void mask_tail_mx(f32x16 (&S)[2], int nb, int g) {
 }
 
 // Key-list window: lane i holds entry first+i of the row's list of key blocks
-// (block id, valid slots, INT8 key scale), so each iteration reads its entry
-// with one readlane instead of a chain of dependent global loads.
+// (block id, valid slots, INT8 key scale) and the block id of entry
+// first+64+i, so each iteration reads the entries it needs (its own and the
+// next two, for the copies) with readlane instead of global loads. A global
+// load inside the loop would make the compiler wait for every outstanding
+// vector-memory operation, including the tile copies still in flight.
 struct KeyWin {
   int kb, nb;
   float dk;
+  int kb_next;
 };
 __device__ inline KeyWin key_window(const uint16_t* list, int first, int count, const int32_t* n_a,
                                     const float* dK, int lane) {
-  KeyWin w{0, kCap, 0.0f};
+  KeyWin w{0, kCap, 0.0f, 0};
   const int e = first + lane;
   if (e < count) {
     w.kb = list[e];
     w.nb = n_a[w.kb];
     w.dk = dK[w.kb];
   }
+  if (e + 64 < count) w.kb_next = list[e + 64];
   // Consume the loaded registers here, so the wait for these loads happens in
   // the (rare) refill and not at every later use of the window.
-  asm volatile("" : "+v"(w.kb), "+v"(w.nb), "+v"(w.dk));
+  asm volatile("" : "+v"(w.kb), "+v"(w.nb), "+v"(w.dk), "+v"(w.kb_next));
   return w;
 }
 __device__ inline int lane_value(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
@@ -337,8 +342,8 @@ __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_
   };
   KeyWin win = key_window(list, 0, n, n_a, dKh, lane);
   // key block of list entry e, first being the current window's first entry
-  auto block_at = [&](int e, int first) -> int {
-    return e - first < 64 ? lane_value(win.kb, e - first) : (int)list[e];
+  auto block_at = [&](int e, int first) -> int {  // e - first < 128
+    return e - first < 64 ? lane_value(win.kb, e - first) : lane_value(win.kb_next, e - first - 64);
   };
   // prologue: logits of block 0, then K(1) and V(0) in flight
   const int kb0 = lane_value(win.kb, 0);
