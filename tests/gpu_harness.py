@@ -128,17 +128,60 @@ def write_ops(buf, p, encs, encs_mx=None):
     buf.ops.copy_(torch.from_numpy(raw))
 
 
-def compare_outputs(O_gpu, O_ref, label):
-    """Parity bar on the rows where O_ref is defined (not NaN)."""
+def compare_outputs(O_gpu, O_ref, label, diag=None):
+    """Parity bar on the rows where O_ref is defined (not NaN). When the bar
+    fails and ``diag`` is given, diag(row indices of O_ref's leading axes)
+    reports the worst rows before the assertion."""
     rows = ~np.isnan(O_ref).any(axis=-1)
     a, b = O_gpu[rows].astype(np.float64), O_ref[rows]
     err = np.abs(a - b)
     max_abs = float(err.max()) if err.size else 0.0
     rel = float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
     log(f"[{label}] rows={int(rows.sum())} max_abs={max_abs:.3e} rel_l2={rel:.3e}")
+    if diag is not None and (max_abs > TOL_MAX_ABS or rel > TOL_REL_L2):
+        row_err = np.where(rows, np.nanmax(np.abs(O_gpu.astype(np.float64) - np.nan_to_num(O_ref)), axis=-1), -1.0)
+        worst = np.argsort(row_err, axis=None)[::-1][:3]
+        diag([np.unravel_index(i, row_err.shape) for i in worst])
     assert max_abs <= TOL_MAX_ABS, (label, max_abs)
     assert rel <= TOL_REL_L2, (label, rel)
     return max_abs, rel
+
+
+def boundary_distance(x, table):
+    """Relative distance of each |x| to the nearest rounding boundary (the
+    midpoint of two neighbouring magnitudes) of a format with value table."""
+    t = np.unique(np.abs(table[np.isfinite(table)]))
+    mids = (t[1:] + t[:-1]) / 2
+    ax = np.abs(np.asarray(x, np.float64))
+    i = np.searchsorted(mids, ax)
+    lo = mids[np.clip(i - 1, 0, mids.size - 1)]
+    hi = mids[np.clip(i, 0, mids.size - 1)]
+    return np.minimum(np.abs(ax - lo), np.abs(ax - hi)) / np.maximum(ax, 1e-300)
+
+
+def flip_report(ops, a, lists, u, label=""):
+    """For query u of region a: the weights whose quantizer input lies closest
+    to a rounding boundary (the NVFP4 2688 P/sigma_P on E2M1, the INT8 path's
+    amplified P on E4M3). A GPU/oracle difference with a distance near float32
+    rounding (about 1e-7) is a rounding flip, not a defect."""
+    from oracle import attention as oatt
+    _, parts = oatt.attend(ops, a, *lists, return_parts=True)
+    Pt = parts["Pt"][u]                                       # [nb, 64]
+    n4, n8 = len(lists[0]), len(lists[1])
+    found = []
+    if n4:
+        g = Pt[:n4].reshape(n4, 4, 16)
+        sigma = formats.e4m3(448.0 * g.max(axis=-1))
+        y = np.where(sigma[..., None] > 0, oatt.FP4_P_SCALE * g / np.where(sigma > 0, sigma, 1.0)[..., None], 0.0)
+        dist = boundary_distance(y, formats.E2M1_VALUES).reshape(n4, 64)
+        found += [(float(dist[j, v]), "nvfp4", int(lists[0][j]), v) for j, v in zip(*np.nonzero(Pt[:n4] > 0))]
+    if n8:
+        y = oatt.AMP * Pt[n4:n4 + n8]
+        dist = boundary_distance(y, formats.e4m3_decode(np.arange(256)))
+        found += [(float(dist[j, v]), "int8", int(lists[1][j]), v) for j, v in zip(*np.nonzero(Pt[n4:n4 + n8] > 0))]
+    found.sort()
+    log(f"  flip report {label} region {a} query {u}: nearest boundaries " +
+        ", ".join(f"{p}:block {b} slot {v} rel {dd:.1e}" for dd, p, b, v in found[:6]))
 
 
 def mask_mismatches(cls_gpu, cls_ref, A_ref, quotas, scope):

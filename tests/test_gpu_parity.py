@@ -15,8 +15,8 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_harness import (SMALL, compare_outputs, expected_sections, inputs, lists_of, log, mask_mismatches,
-                         problem_of, sections, to_device, write_lists, write_ops)
+from gpu_harness import (SMALL, compare_outputs, expected_sections, flip_report, inputs, lists_of, log,
+                         mask_mismatches, problem_of, sections, to_device, write_lists, write_ops)
 from oracle import attention as oatt, draft as odraft, encode as oenc, partition, pipeline, rank as orank
 from paper_2609_32628_amd import api
 from synth import configs
@@ -204,11 +204,21 @@ def test_mixed_attn_injected(w, budgets16):
     Og = O.cpu().numpy().reshape(-1, w.N, w.d)
     assert not np.isnan(Og).any()
     ref = np.empty_like(Og, dtype=np.float64)
+    all_ops = []
     for bh, (enc, cls) in enumerate(zip(encs, clss)):
         ops = oatt.Operands.quantized(oenc.reconstruct(enc), n_a)
+        all_ops.append(ops)
         for a in range(n_a.size):
             ref[bh, slot2tok[a * 64:a * 64 + n_a[a]]] = oatt.attend(ops, a, *orank.key_lists_all(cls[a]))
-    compare_outputs(Og, ref, f"{w.name} {num16} {budgets}")
+    tok2slot = np.full(w.N, -1)
+    tok2slot[slot2tok[slot2tok >= 0]] = np.nonzero(slot2tok >= 0)[0]
+
+    def diag(worst):
+        for bh, tok in worst:
+            slot = tok2slot[tok]
+            flip_report(all_ops[bh], slot // 64, orank.key_lists_all(clss[bh][slot // 64]), slot % 64, f"head {bh}")
+
+    compare_outputs(Og, ref, f"{w.name} {num16} {budgets}", diag)
 
 
 @pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
