@@ -260,6 +260,10 @@ E2E_CASES = CASES + [replace(SMALL, name="small-16bit-15/10/30", num16=15), SMAL
 def test_end_to_end(w):
     log(f"end-to-end parity {w.name}")
     Q, K, V = inputs(w)
+    _check_end_to_end(w, Q, K, V)
+
+
+def _check_end_to_end(w, Q, K, V):
     buf, p, O = _run_gpu(w, Q, K, V)
     layout, outs = pipeline.run(w, Q, K, V)
     slot2tok, n_a, _ = layout
@@ -278,6 +282,38 @@ def test_end_to_end(w):
                 ref[slot2tok[a * 64:a * 64 + n_a[a]]] = np.nan
         log(f"  head {bh}: near-tie mask mismatches {n_bad}")
         compare_outputs(Og[bh], ref, f"{w.name} head {bh}")
+
+
+def _degenerate(case):
+    """Inputs of the degenerate cases: tiny frames (one short block each),
+    single-token frames, all-zero Q and K (uniform draft map, every score
+    tied), all-zero V, and constant Q, K, V."""
+    if case == "frames-3x1x5":
+        w = configs.Workload(case, B=1, H=2, d=64, T=3, Hg=1, Wg=5, dtype="fp32", budgets=(30, 30, 100),
+                             scope="head", head_scale=False, seed=21)
+        return w, inputs(w)
+    if case == "frames-4x1x1":
+        w = configs.Workload(case, B=1, H=1, d=128, T=4, Hg=1, Wg=1, dtype="bf16", budgets=(25, 50, 100),
+                             scope="row", head_scale=True, seed=22)
+        return w, inputs(w)
+    base, fmt4 = (case[:-6], "mxfp4") if case.endswith("-mxfp4") else (case, "nvfp4")
+    w = replace(SMALL, name=case, fmt4=fmt4)
+    Q, K, V = inputs(w)
+    if base == "zero-qk":
+        Q, K = np.zeros_like(Q), np.zeros_like(K)
+    elif base == "zero-v":
+        V = np.zeros_like(V)
+    elif base == "constant":
+        Q, K, V = np.ones_like(Q), np.ones_like(K), np.ones_like(V)
+    return w, (Q, K, V)
+
+
+@pytest.mark.parametrize("case", ["frames-3x1x5", "frames-4x1x1", "zero-qk", "zero-v", "constant",
+                                  "zero-qk-mxfp4", "constant-mxfp4"])
+def test_degenerate_inputs(case):
+    log(f"end-to-end parity, degenerate case {case}")
+    w, (Q, K, V) = _degenerate(case)
+    _check_end_to_end(w, Q, K, V)
 
 
 def test_mid_layer_sampled_rows():
