@@ -3,7 +3,8 @@
 //
 // One workgroup of two waves owns one query block a (64 query slots); wave w
 // owns the 32-query tile qt = w. The workgroup walks the block's retained key
-// blocks: the NVFP4 ones in ascending order, then the INT8 ones, then the
+// blocks: the 4-bit ones in ascending order (NVFP4, or MXFP4 when the
+// operands were prepared in that encoding), then the INT8 ones, then the
 // 16-bit ones. All blocks share the fp32 running maxima m, the denominators l
 // and the numerator U.
 //
@@ -19,8 +20,9 @@
 //
 // Units: the NVFP4 phase multiplies fp16 sigma*e operands, so U carries a
 // factor 2688/g_V and l the unamplified weights (the MXFP4 alternative of the
-// 4-bit phase runs scaled fp4 MFMAs and stays in the common units); Enter converts to the 8-bit path's
-// units U_c / (eta delta_c), l / eta; the 8-bit phase accumulates amplified
+// 4-bit phase runs scaled fp4 MFMAs and stays in the common units); Enter
+// converts to the 8-bit path's units U_c / (eta delta_c), l / eta; the 8-bit
+// phase accumulates amplified
 // weights 2^(z - m + 8.807) and E4M3 codes; Exit converts back; the 16-bit
 // phase then accumulates fp16 weights times fp16 values in the common units.
 //

@@ -15,7 +15,10 @@
 //   NVFP4 Q, K (16-channel groups) and V (16-slot groups) as the exact fp16
 //   value sigma*e,
 //   and, when asked for, the half-precision Q, K, V of the 16-bit path in the
-//   same fragment order as the NVFP4 sections.
+//   same fragment order as the NVFP4 sections;
+//   with the MXFP4 encoding instead of NVFP4: E2M1 codes of 32-element blocks
+//   (channels for Q and K, key slots for V) with E8M0 scale words, in the
+//   operand order of the scaled fp4 MFMA.
 // Scale arithmetic is float32 with one rounding per operation in the documented
 // order (the build uses -ffp-contract=off); division by a scale is a
 // multiplication by its correctly rounded float32 reciprocal. The E2M1 and E4M3
