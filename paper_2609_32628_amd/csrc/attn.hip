@@ -35,6 +35,8 @@
 // v_cvt_scalef32_pk_fp4_f32 / v_cvt_scalef32_pk_f16_fp4 (E2M1 and back, unit
 // scales); both round to nearest even, which the device format tests check
 // against the format definitions.
+#include <utility>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -48,14 +50,22 @@ __device__ inline float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
 // Asynchronous copy of one 1 KB operand fragment (16 bytes per lane, lane
-// order) from global memory to LDS at the wave-uniform address dst. Issued as
-// inline assembly so that the compiler does not add its conservative
+// order) from global memory to LDS. The source is tile + voff + OFS with the
+// wave-uniform tile address in scalar registers and voff = 16 * lane, so the
+// address needs no vector arithmetic; the destination is lds + OFS (the
+// instruction adds its immediate offset to the LDS address in M0 as well).
+// Issued as inline assembly so that the compiler does not add its conservative
 // "wait for every LDS copy" before later LDS reads; the kernel waits for
 // exactly the copies it needs (wait_vmem_keep) instead.
-__device__ inline void dma_fragment(const void* src_lane, void* dst) {
-  const uint32_t lds = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr)dst)));
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src_lane), "s"(lds)
+template <int OFS>
+__device__ inline void dma_fragment(const void* tile, uint32_t voff, uint32_t lds) {
+  static_assert(OFS >= 0 && OFS < 4096, "immediate offset out of range");
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 offset:%3" ::"v"(voff), "s"(tile),
+               "s"(lds), "n"(OFS)
                : "memory", "m0");
+}
+__device__ inline uint32_t lds_address(void* p) {
+  return __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr)p)));
 }
 __device__ inline void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 __device__ inline void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
@@ -330,17 +340,17 @@ __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_
                                   FIRST first_qk, STEP1 region1, STEP2 region2, PV pv) {
   constexpr int TILE = NFK * 64;       // fragments per tile
   constexpr int W0 = (NFK + 1) / 2;    // fragments wave 0 copies; wave 1 copies the rest
+  // Wave 0 copies fragments [0, W0) of a tile, wave 1 the rest; fragment i of
+  // a wave's share sits 1 KB * i after its first one, in both memories (4 KB
+  // steps of the scalar bases, the remainder as the immediate offset).
+  const uint32_t voff = 16u * static_cast<uint32_t>(lane);
+  const int f0 = wave ? W0 : 0, nf = wave ? NFK - W0 : W0;
   auto dma_tile = [&](const Frag* src, Frag* dst) {
-    if constexpr (NFK % 2 == 0) {
-#pragma unroll
-      for (int f = wave * W0; f < (wave + 1) * W0; ++f) dma_fragment(src + f * 64 + lane, dst + f * 64);
-    } else {
-#pragma unroll
-      for (int i = 0; i < W0; ++i) {
-        const int f = wave ? W0 + i : i;
-        if (f < NFK) dma_fragment(src + f * 64 + lane, dst + f * 64);
-      }
-    }
+    const char* base = reinterpret_cast<const char*>(src + f0 * 64);
+    const uint32_t lds = lds_address(dst + f0 * 64);
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      ((I < nf ? dma_fragment<(I % 4) * 1024>(base + (I / 4) * 4096, voff, lds + (I / 4) * 4096) : void()), ...);
+    }(std::make_integer_sequence<int, W0>{});
   };
   KeyWin win = key_window(list, 0, n, n_a, dKh, lane);
   // key block of list entry e, first being the current window's first entry
