@@ -76,12 +76,19 @@ __device__ inline void rescale(f32x16 (&U)[NT], float alpha) {
   for (int t = 0; t < NT; ++t) U[t] *= alpha;
 }
 
+// Maximum of v over lanes l and l ^ 32: one v_permlane32_swap hands each lane
+// both halves' values (no LDS permute, so no wait on the tile reads in flight).
+__device__ inline float max_halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // Running-max update for one 32-query tile: bm_lane is this lane's maximum raw
 // logit of the block (-inf on padding), scale converts raw logits to log2
 // units. Updates m and l, returns the new maximum and (via alpha) the factor
 // 2^(m_old - m_new) that the numerator still has to be multiplied by.
 __device__ inline float new_max(float bm_lane, float scale, float& m, float& l, float& alpha) {
-  const float bm = fmaxf(bm_lane, __shfl_xor(bm_lane, 32, 64));
+  const float bm = max_halves(bm_lane);
   const float mn = fmaxf(m, bm * scale);
   alpha = exp2_fast(m - mn);
   m = mn;
