@@ -41,6 +41,18 @@ __global__ void rank_init_kernel(RankArgs args) {
   }
 }
 
+// Histogram slot of each cut in this pass: -1 for a finished cut, else the
+// first active cut with the same prefix (cuts with equal prefixes, such as all
+// of them in the first pass, count the same elements into one histogram).
+__device__ inline void hist_slots(const RankArgs& args, int bh, int hi, int (&slot)[kCuts], uint64_t (&pre)[kCuts]) {
+  for (int t = 0; t < kCuts; ++t) {
+    pre[t] = args.prefix[bh * kCuts + t] >> hi;
+    slot[t] = args.kleft[bh * kCuts + t] > 0 ? t : -1;
+    for (int u = 0; u < t && slot[t] == t; ++u)
+      if (slot[u] == u && pre[u] == pre[t]) slot[t] = u;
+  }
+}
+
 __global__ __launch_bounds__(256) void rank_hist_kernel(RankArgs args, int pass) {
   __shared__ uint32_t lh[kCuts][kBins];
   const int bh = blockIdx.y;
@@ -48,31 +60,44 @@ __global__ __launch_bounds__(256) void rank_hist_kernel(RankArgs args, int pass)
   const int sh = kShift[pass], hi = sh + kWidth[pass];
   const uint64_t mask = (1ull << kWidth[pass]) - 1ull;
   for (int i = threadIdx.x; i < kCuts * kBins; i += 256) (&lh[0][0])[i] = 0u;
-  bool act[kCuts], any = false;
+  int slot[kCuts];
   uint64_t pre[kCuts];
+  hist_slots(args, bh, hi, slot, pre);
+  bool own[kCuts], any = false;
   for (int t = 0; t < kCuts; ++t) {
-    act[t] = args.kleft[bh * kCuts + t] > 0;
-    pre[t] = args.prefix[bh * kCuts + t] >> hi;
-    any = any || act[t];
+    own[t] = slot[t] == t;
+    any = any || own[t];
   }
   __syncthreads();
   if (any) {
     const float* A = args.A + (int64_t)bh * M;
     const int64_t e0 = (int64_t)blockIdx.x * kHistChunk;
     const int64_t e1 = e0 + kHistChunk < M ? e0 + kHistChunk : M;
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += 256) {
-      const uint64_t key = rank_key(A[e], static_cast<uint32_t>(e));
-      const uint32_t dig = static_cast<uint32_t>((key >> sh) & mask);
+    constexpr int U = 8;  // loads in flight per thread
+    for (int64_t eb = e0 + threadIdx.x; eb < e1; eb += 256 * U) {
+      float v[U];
 #pragma unroll
-      for (int t = 0; t < kCuts; ++t)
-        if (act[t] && (key >> hi) == pre[t]) atomicAdd(&lh[t][dig], 1u);
+      for (int u = 0; u < U; ++u) v[u] = eb + u * 256 < e1 ? A[eb + u * 256] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int64_t e = eb + u * 256;
+        if (e >= e1) break;
+        const uint64_t key = rank_key(v[u], static_cast<uint32_t>(e));
+        const uint32_t dig = static_cast<uint32_t>((key >> sh) & mask);
+#pragma unroll
+        for (int t = 0; t < kCuts; ++t)
+          if (own[t] && (key >> hi) == pre[t]) atomicAdd(&lh[t][dig], 1u);
+      }
     }
   }
   __syncthreads();
   uint32_t* gh = args.hist + (int64_t)bh * kCuts * kBins;
-  for (int i = threadIdx.x; i < kCuts * kBins; i += 256) {
-    uint32_t v = (&lh[0][0])[i];
-    if (v) atomicAdd(gh + i, v);
+  for (int t = 0; t < kCuts; ++t) {
+    if (!own[t]) continue;  // uniform across the block
+    for (int i = threadIdx.x; i < kBins; i += 256) {
+      const uint32_t v = lh[t][i];
+      if (v) atomicAdd(gh + t * kBins + i, v);
+    }
   }
 }
 
@@ -98,13 +123,17 @@ __global__ __launch_bounds__(256) void rank_scan_kernel(RankArgs args, int pass)
   const int bh = blockIdx.x;
   const int s = kShift[pass];
   uint32_t* gh = args.hist + (int64_t)bh * kCuts * kBins;
+  // the histogram slots of this pass, fixed before any cut's prefix changes
+  int slot[kCuts];
+  uint64_t pre[kCuts];
+  hist_slots(args, bh, s + kWidth[pass], slot, pre);
   for (int t = 0; t < kCuts; ++t) {
     const int64_t k = args.kleft[bh * kCuts + t];
     if (k <= 0) continue;  // uniform across the block
     // thread i owns bins [2047-8i-7, 2047-8i], visited from the top
     uint32_t c[8], local = 0;
     for (int q = 0; q < 8; ++q) {
-      c[q] = gh[t * kBins + (kBins - 1 - 8 * threadIdx.x - q)];
+      c[q] = gh[slot[t] * kBins + (kBins - 1 - 8 * threadIdx.x - q)];
       local += c[q];
     }
     uint32_t total;
@@ -160,49 +189,77 @@ __global__ __launch_bounds__(256) void rank_row_select_kernel(RankArgs args, int
   }
 }
 
+// Exclusive prefix sum of 64-bit values over a 256-thread block.
+__device__ inline uint64_t block_exscan_256_u64(uint64_t v, uint64_t* sh, uint64_t* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint64_t x = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[w] = x;
+  __syncthreads();
+  uint64_t base = 0;
+  for (int q = 0; q < w; ++q) base += sh[q];
+  *total = sh[0] + sh[1] + sh[2] + sh[3];
+  __syncthreads();
+  return base + x - v;
+}
+
 // Classes, ascending per-row lists (4-bit, then 8-bit, then 16-bit: the phase
-// order of the attention), counts and row cost.
+// order of the attention), counts and row cost. Thread i owns the contiguous
+// run of key blocks [i E, (i + 1) E), E = ceil(R / 256): it classifies its run,
+// one block-wide scan of the packed per-class counts (21 bits each) gives every
+// class's write offset, and a second walk over the run writes the lists.
 __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
-  __shared__ uint32_t sh[4];
+  __shared__ uint64_t sh[4];
   const int a = blockIdx.x, bh = blockIdx.y, R = args.R;
   const int64_t row = (int64_t)bh * R + a;
   const float* A = args.A + row * R;
-  const uint64_t* thr = args.scope == DA2_SCOPE_HEAD ? args.thr + (int64_t)bh * kCuts : args.thr + row * kCuts;
+  const bool head = args.scope == DA2_SCOPE_HEAD;
+  const uint64_t* thr = head ? args.thr + (int64_t)bh * kCuts : args.thr + row * kCuts;
   const uint64_t t16 = thr[0], t8 = thr[1], t4 = thr[2];
   uint8_t* cls = args.cls + row * R;
   uint16_t* keys = args.keys + row * R;
-  const int lane = threadIdx.x & 63;
-  uint32_t n[3] = {0u, 0u, 0u};  // n4, n8, n16
-  uint32_t base = 0;
-  for (int phase = 0; phase < 3; ++phase) {
-    const int want = 4 << phase;
-    const uint32_t start = base;
-    for (int c0 = 0; c0 < R; c0 += 256) {
-      const int b = c0 + threadIdx.x;
-      int c = 0;
-      if (b < R) {
-        const uint64_t key = args.scope == DA2_SCOPE_HEAD ? rank_key(A[b], static_cast<uint32_t>(a * R + b))
-                                                          : rank_key(A[b], static_cast<uint32_t>(b));
-        c = key >= t16 ? 16 : (key >= t8 ? 8 : (key >= t4 ? 4 : 0));
-        if (phase == 0) cls[b] = static_cast<uint8_t>(c);
-      }
-      const bool f = c == want;
-      const uint64_t m = __ballot(f);
-      const uint32_t in_wave = __popcll(m & ((1ull << lane) - 1ull));
-      uint32_t tot;
-      const uint32_t wave_base = block_exscan_256(lane == 0 ? (uint32_t)__popcll(m) : 0u, sh, &tot);
-      const uint32_t wb = __shfl(wave_base, 0, 64);
-      if (f) keys[base + wb + in_wave] = static_cast<uint16_t>(b);
-      base += tot;
-    }
-    n[phase] = base - start;
+  auto class_of = [&](int b) -> int {
+    const uint64_t key = head ? rank_key(A[b], static_cast<uint32_t>(a * R + b)) : rank_key(A[b], static_cast<uint32_t>(b));
+    return key >= t16 ? 16 : (key >= t8 ? 8 : (key >= t4 ? 4 : 0));
+  };
+  constexpr int kF = 21;
+  constexpr uint64_t kM = (1ull << kF) - 1ull;
+  auto field = [](int c) -> uint64_t {
+    return c == 4 ? 1ull : (c == 8 ? (1ull << kF) : (c == 16 ? (1ull << (2 * kF)) : 0ull));
+  };
+  const int E = (R + 255) / 256;
+  const int b0 = min(R, static_cast<int>(threadIdx.x) * E), b1 = min(R, b0 + E);
+  uint64_t cnt = 0;
+  for (int b = b0; b < b1; ++b) {
+    const int c = class_of(b);
+    cls[b] = static_cast<uint8_t>(c);
+    cnt += field(c);
+  }
+  uint64_t tot;
+  const uint64_t before = block_exscan_256_u64(cnt, sh, &tot);
+  const uint32_t n4 = static_cast<uint32_t>(tot & kM), n8 = static_cast<uint32_t>((tot >> kF) & kM),
+                 n16 = static_cast<uint32_t>((tot >> (2 * kF)) & kM);
+  uint32_t p4 = static_cast<uint32_t>(before & kM);
+  uint32_t p8 = n4 + static_cast<uint32_t>((before >> kF) & kM);
+  uint32_t p16 = n4 + n8 + static_cast<uint32_t>((before >> (2 * kF)) & kM);
+  for (int b = b0; b < b1; ++b) {
+    const int c = class_of(b);
+    if (c == 4)
+      keys[p4++] = static_cast<uint16_t>(b);
+    else if (c == 8)
+      keys[p8++] = static_cast<uint16_t>(b);
+    else if (c == 16)
+      keys[p16++] = static_cast<uint16_t>(b);
   }
   if (threadIdx.x == 0) {
-    args.counts[row * 4 + 0] = n[0];
-    args.counts[row * 4 + 1] = n[1];
-    args.counts[row * 4 + 2] = n[2];
+    args.counts[row * 4 + 0] = n4;
+    args.counts[row * 4 + 1] = n8;
+    args.counts[row * 4 + 2] = n16;
     args.counts[row * 4 + 3] = 0;
-    args.cost[row] = 5 * n[0] + 4 * n[1] + 5 * n[2];
+    args.cost[row] = 5 * n4 + 4 * n8 + 5 * n16;
   }
 }
 
@@ -237,18 +294,18 @@ __global__ __launch_bounds__(1024) void rank_order_kernel(RankArgs args) {
   constexpr int per = kOrderBins / 1024;
   uint32_t s = 0;
   for (int q = 0; q < per; ++q) s += hist[threadIdx.x * per + q];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t run = 0;
-    for (int q = 0; q < 1024; ++q) {
-      uint32_t v = part[q];
-      part[q] = run;
-      run += v;
-    }
+  // exclusive scan of the 1024 per-thread sums: within each wave, then over
+  // the 16 wave totals
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t x = s;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
   }
+  if (lane == 63) part[w] = x;
   __syncthreads();
-  uint32_t run = part[threadIdx.x];
+  uint32_t run = x - s;
+  for (int q = 0; q < w; ++q) run += part[q];
   for (int q = 0; q < per; ++q) {
     uint32_t v = hist[threadIdx.x * per + q];
     hist[threadIdx.x * per + q] = run;
