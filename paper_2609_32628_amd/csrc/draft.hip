@@ -3,8 +3,8 @@
 //   draft_pool     one workgroup per (block, head, Q or K): mean (float64 sum /
 //                  n_a) and channel max over the valid tokens, plus the per-head
 //                  max|Q|, max|K| used by the NVFP4 tensor scales.
-//   draft_logits   64x64 tiles of Qbar Kbar^T / sqrt d or Qmax Kmax^T / sqrt d on
-//                  the float64 matrix cores (16x16x4 MFMA).
+//   draft_logits   128x128 tiles of Qbar Kbar^T / sqrt d or Qmax Kmax^T / sqrt d
+//                  on the float64 matrix cores (16x16x4 MFMA).
 //   draft_softmax  one wave per row: the two row softmaxes (max subtracted)
 //                  mixed with weight lambda, rounded once to float32.
 #include "common.hpp"
@@ -96,38 +96,39 @@ __global__ __launch_bounds__(256) void draft_pool_kernel(DraftArgs args) {
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-// One 64x64 logit tile of one branch (blockIdx.z = 2*head + branch) on the
-// float64 matrix cores: each wave owns a 32x32 quarter as 2x2 MFMA tiles of
-// 16x16x4. The reduction over channels may visit them in any order as long as
-// both operands agree: lane group q = lane/16 of k-step 2t+h reads channel
-// 8t + 2q + h, so one 16-byte load per operand tile feeds two k-steps. The
-// loads run one group of 8 channels ahead of the MFMAs, and the four
-// accumulators are updated in turn so that consecutive MFMAs are independent.
-// Rows and columns beyond R read row R-1 and are not stored.
+// One 128x128 logit tile of one branch (blockIdx.z = 2*head + branch) on the
+// float64 matrix cores: each wave owns a 64x64 quarter as 4x4 MFMA tiles of
+// 16x16x4, so every operand value loaded feeds four MFMAs. The reduction over
+// channels may visit them in any order as long as both operands agree: lane
+// group q = lane/16 of k-step 2t+h reads channel 8t + 2q + h, so one 16-byte
+// load per operand tile feeds two k-steps. The loads run one group of 8
+// channels ahead of the MFMAs, and consecutive MFMAs update different
+// accumulators. Rows and columns beyond R read row R-1 and are not stored.
+constexpr int kLogitTile = 128;
 template <int D>
 __global__ __launch_bounds__(256) void draft_logits_kernel(DraftArgs args) {
-  constexpr int d = D;
+  constexpr int d = D, NI = 4;
   const int R = args.R, bh = blockIdx.z >> 1, br = blockIdx.z & 1;
   const double* Qs = (br == 0 ? args.Qbar : args.Qmax) + (int64_t)bh * R * d;
   const double* Ks = (br == 0 ? args.Kbar : args.Kmax) + (int64_t)bh * R * d;
   double* out = (br == 0 ? args.S1 : args.S2) + (int64_t)bh * R * R;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, li = lane & 15, q = lane >> 4;
-  const int r0 = blockIdx.y * 64 + (wave >> 1) * 32, c0 = blockIdx.x * 64 + (wave & 1) * 32;
-  const double* pa[2];
-  const double* pb[2];
+  const int r0 = blockIdx.y * kLogitTile + (wave >> 1) * 64, c0 = blockIdx.x * kLogitTile + (wave & 1) * 64;
+  const double* pa[NI];
+  const double* pb[NI];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < NI; ++i) {
     pa[i] = Qs + (int64_t)min(r0 + 16 * i + li, R - 1) * d + 2 * q;
     pb[i] = Ks + (int64_t)min(c0 + 16 * i + li, R - 1) * d + 2 * q;
   }
-  f64x4 acc[2][2];
+  f64x4 acc[NI][NI];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
-  double2 a[2][2], b[2][2];  // [buffer][tile]
+    for (int j = 0; j < NI; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+  double2 a[2][NI], b[2][NI];  // [buffer][tile]
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < NI; ++i) {
     a[0][i] = *reinterpret_cast<const double2*>(pa[i]);
     b[0][i] = *reinterpret_cast<const double2*>(pb[i]);
   }
@@ -136,28 +137,28 @@ __global__ __launch_bounds__(256) void draft_logits_kernel(DraftArgs args) {
     const int cur = t & 1;
     if (t + 1 < d / 8) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < NI; ++i) {
         a[cur ^ 1][i] = *reinterpret_cast<const double2*>(pa[i] + 8 * (t + 1));
         b[cur ^ 1][i] = *reinterpret_cast<const double2*>(pb[i] + 8 * (t + 1));
       }
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NI; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[cur][i].x, b[cur][j].x, acc[i][j], 0, 0, 0);
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NI; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[cur][i].y, b[cur][j].y, acc[i][j], 0, 0, 0);
   }
   // accumulator element e of lane l: row l/16 + 4e, column l%16
   const double sqd = sqrt((double)d);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NI; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int row = r0 + 16 * i + q + 4 * e, col = c0 + 16 * j + li;
@@ -257,7 +258,7 @@ hipError_t launch_draft(const DraftArgs& args, hipStream_t stream) {
     else
       hipLaunchKernelGGL((draft_pool_kernel<64, float>), pool_grid, dim3(256), 0, stream, args);
   }
-  const int nt = (args.R + 63) / 64;
+  const int nt = (args.R + kLogitTile - 1) / kLogitTile;
   if (args.d == 128)
     hipLaunchKernelGGL(draft_logits_kernel<128>, dim3(nt, nt, 2 * BH), dim3(256), 0, stream, args);
   else

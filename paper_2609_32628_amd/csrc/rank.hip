@@ -207,22 +207,28 @@ __device__ inline uint64_t block_exscan_256_u64(uint64_t v, uint64_t* sh, uint64
 }
 
 // Classes, ascending per-row lists (4-bit, then 8-bit, then 16-bit: the phase
-// order of the attention), counts and row cost. Thread i owns the contiguous
-// run of key blocks [i E, (i + 1) E), E = ceil(R / 256): it classifies its run,
-// one block-wide scan of the packed per-class counts (21 bits each) gives every
-// class's write offset, and a second walk over the run writes the lists.
+// order of the attention), counts and row cost. The row's scores are staged in
+// LDS (R floats, dynamic) with coalesced loads; thread i then owns the
+// contiguous run of key blocks [i E, (i + 1) E), E = ceil(R / 256): it
+// classifies its run, one block-wide scan of the packed per-class counts (21
+// bits each) gives every class's write offset, and a second walk over the run
+// writes the lists.
 __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
+  extern __shared__ float srow[];
   __shared__ uint64_t sh[4];
   const int a = blockIdx.x, bh = blockIdx.y, R = args.R;
   const int64_t row = (int64_t)bh * R + a;
   const float* A = args.A + row * R;
+  for (int b = threadIdx.x; b < R; b += 256) srow[b] = A[b];
+  __syncthreads();
   const bool head = args.scope == DA2_SCOPE_HEAD;
   const uint64_t* thr = head ? args.thr + (int64_t)bh * kCuts : args.thr + row * kCuts;
   const uint64_t t16 = thr[0], t8 = thr[1], t4 = thr[2];
   uint8_t* cls = args.cls + row * R;
   uint16_t* keys = args.keys + row * R;
   auto class_of = [&](int b) -> int {
-    const uint64_t key = head ? rank_key(A[b], static_cast<uint32_t>(a * R + b)) : rank_key(A[b], static_cast<uint32_t>(b));
+    const uint64_t key =
+        head ? rank_key(srow[b], static_cast<uint32_t>(a * R + b)) : rank_key(srow[b], static_cast<uint32_t>(b));
     return key >= t16 ? 16 : (key >= t8 ? 8 : (key >= t4 ? 4 : 0));
   };
   constexpr int kF = 21;
@@ -334,7 +340,7 @@ hipError_t launch_rank(const RankArgs& args, hipStream_t stream) {
     while (P < args.R) P <<= 1;
     hipLaunchKernelGGL(rank_row_select_kernel, dim3(args.R, BH), dim3(256), P * sizeof(uint64_t), stream, args, P);
   }
-  hipLaunchKernelGGL(rank_classify_kernel, dim3(args.R, BH), dim3(256), 0, stream, args);
+  hipLaunchKernelGGL(rank_classify_kernel, dim3(args.R, BH), dim3(256), args.R * sizeof(float), stream, args);
   hipLaunchKernelGGL(rank_order_kernel, dim3(1), dim3(1024), 0, stream, args);
   return hipGetLastError();
 }
