@@ -24,9 +24,9 @@ FLAGS = [
 ]
 
 
-# The attention kernel never produces NaN (finite operands, -inf only for masked
-# logits), so max/min need no NaN canonicalization there.
-EXTRA = {"attn.hip": ["-fno-honor-nans"]}
+# The attention and draft kernels never produce NaN (finite operands, -inf only
+# for masked logits and padding), so max/min need no NaN canonicalization there.
+EXTRA = {"attn.hip": ["-fno-honor-nans"], "draft.hip": ["-fno-honor-nans"]}
 
 
 def _compile(src):

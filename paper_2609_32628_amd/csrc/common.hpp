@@ -62,6 +62,40 @@ __device__ inline void load_chunk(const float* p, float* x) {
   x[2] = v.z;
   x[3] = v.w;
 }
+// All ones for a valid lane, else zero. The empty asm hides how the mask was
+// made, so a load masked with it is not turned back into a branch around the
+// load (which would serialize the loads that are meant to overlap).
+__device__ inline uint32_t lane_mask(bool valid) {
+  uint32_t m = valid ? 0xFFFFFFFFu : 0u;
+  asm("" : "+v"(m));
+  return m;
+}
+__device__ inline uint4 masked(const uint4& v, uint32_t m) { return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m); }
+
+// The same for a 16-byte chunk already in registers (T selects bf16 or fp32).
+template <typename T>
+__device__ inline void chunk_floats(const uint4& v, float* x) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = __uint_as_float(w[i]);
+  }
+}
+
+// Two channels (2p, 2p+1) of row s of a [rows][D] tile in LDS, as floats.
+__device__ inline float2 tile_pair(const uint16_t* tile, int D, int s, int p) {
+  const uint32_t w = reinterpret_cast<const uint32_t*>(tile + s * D)[p];
+  return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+}
+__device__ inline float2 tile_pair(const float* tile, int D, int s, int p) {
+  return reinterpret_cast<const float2*>(tile + s * D)[p];
+}
 
 // ---- E4M3 ------------------------------------------------------------------
 // Value of a >= 0 after a round-to-nearest-even cast to E4M3 (saturating).

@@ -18,72 +18,77 @@ __global__ void zero_u32_kernel(uint32_t* p, int64_t stride, int count, int64_t 
   (void)n_rows;
 }
 
-// One workgroup per (block, head, Q or K). Thread (row group rg, chunk cc)
-// reads 16-byte chunks of the block's valid slots rg, rg + RG, ...; the
-// per-channel float64 sums and float32 maxima are reduced across row groups
-// (lanes CPR apart, then the four waves through LDS).
+// One workgroup per (block, head, Q or K). The block's slots are read with
+// coalesced 16-byte loads into an LDS tile (padding rows repeat the last valid
+// row); thread
+// (channel pair p, row group q) then reduces rows [q RPQ, (q + 1) RPQ) of its
+// two channels: float64 sums, float32 maxima over the valid rows and max |x|.
+// The row groups are combined through LDS in order. Sums of bf16 values in
+// float64 are exact, so for bf16 inputs the order of the additions does not
+// change the mean.
 template <int D, typename T>
 __global__ __launch_bounds__(256) void draft_pool_kernel(DraftArgs args) {
-  constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte load
-  constexpr int CPR = D / EPC;         // loads per slot row
-  constexpr int RG = 256 / CPR;        // row groups
-  constexpr int RPT = kCap / RG;       // rows per thread
-  __shared__ double s_sum[4][D];
-  __shared__ float s_max[4][D];
+  constexpr int EPC = 16 / sizeof(T);    // elements per 16-byte load
+  constexpr int CPR = D / EPC;           // loads per slot row
+  constexpr int LPT = kCap * CPR / 256;  // loads per thread
+  constexpr int CP = D / 2;              // channel pairs
+  constexpr int RQ = 256 / CP;           // row groups of the reduction
+  constexpr int RPQ = kCap / RQ;         // rows per group
+  __shared__ __align__(16) T tile[kCap * D];
+  __shared__ double s_sum[RQ][D];
+  __shared__ float s_max[RQ][D];
   __shared__ float s_amax[4];
   const int a = blockIdx.x, bh = blockIdx.y, which = blockIdx.z;
   const int b = bh / args.H, h = bh % args.H, tid = threadIdx.x;
   const Layout L = layout_view(args.layout, args.R, args.Npad);
   const int n = L.n_a[a];
   const int32_t* slots = L.slot2tok + (int64_t)a * kCap;
-  const int cc = tid % CPR, rg = tid / CPR;
-  const T* X = static_cast<const T*>(which == 0 ? args.Q : args.K) + (int64_t)b * args.sb + (int64_t)h * args.sh +
-               cc * EPC;
-  float x[RPT][EPC];
+  const T* X = static_cast<const T*>(which == 0 ? args.Q : args.K) + (int64_t)b * args.sb + (int64_t)h * args.sh;
+  // token indices first, then the data loads, all unconditional so that they
+  // overlap: padding slots read the last valid row again (a copy changes no
+  // maximum; the sums skip those rows)
+  int tok[LPT];
 #pragma unroll
-  for (int k = 0; k < RPT; ++k) {
-    const int s = rg + RG * k;
-    if (s < n) load_chunk(X + (int64_t)slots[s] * args.sn, x[k]);
-  }
-  double sum[EPC];
-  float mx[EPC];
-  float amax = 0.0f;
+  for (int k = 0; k < LPT; ++k) tok[k] = slots[min((tid + 256 * k) / CPR, n - 1)];
+  uint4 v[LPT];
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) {
-    sum[e] = 0.0;
-    mx[e] = -INFINITY;
+  for (int k = 0; k < LPT; ++k) {
+    const int cc = (tid + 256 * k) % CPR;
+    v[k] = *reinterpret_cast<const uint4*>(X + (int64_t)tok[k] * args.sn + cc * EPC);
   }
 #pragma unroll
-  for (int k = 0; k < RPT; ++k) {
-    if (rg + RG * k < n) {
+  for (int k = 0; k < LPT; ++k) reinterpret_cast<uint4*>(tile)[tid + 256 * k] = v[k];
+  __syncthreads();
+  const int p = tid % CP, q = tid / CP;
+  double s0 = 0.0, s1 = 0.0;
+  float m0 = -INFINITY, m1 = -INFINITY, am = 0.0f;
 #pragma unroll
-      for (int e = 0; e < EPC; ++e) {
-        sum[e] += (double)x[k][e];
-        mx[e] = fmaxf(mx[e], x[k][e]);
-        amax = fmaxf(amax, fabsf(x[k][e]));
-      }
+  for (int r = 0; r < RPQ; ++r) {
+    const int s = q * RPQ + r;
+    const float2 f = tile_pair(tile, D, s, p);
+    if (s < n) {
+      s0 += (double)f.x;
+      s1 += (double)f.y;
     }
+    m0 = fmaxf(m0, f.x);
+    m1 = fmaxf(m1, f.y);
+    am = fmaxf(am, fmaxf(fabsf(f.x), fabsf(f.y)));
   }
-#pragma unroll
-  for (int o = CPR; o < 64; o <<= 1)
-#pragma unroll
-    for (int e = 0; e < EPC; ++e) {
-      sum[e] += __shfl_xor(sum[e], o, 64);
-      mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], o, 64));
-    }
-  const int w = tid >> 6, lane = tid & 63;
-  if (lane < CPR)
-#pragma unroll
-    for (int e = 0; e < EPC; ++e) {
-      s_sum[w][cc * EPC + e] = sum[e];
-      s_max[w][cc * EPC + e] = mx[e];
-    }
-  amax = wave_max(amax);
-  if (lane == 0) s_amax[w] = amax;
+  s_sum[q][2 * p] = s0;
+  s_sum[q][2 * p + 1] = s1;
+  s_max[q][2 * p] = m0;
+  s_max[q][2 * p + 1] = m1;
+  am = wave_max(am);
+  if ((tid & 63) == 0) s_amax[tid >> 6] = am;
   __syncthreads();
   if (tid < D) {
-    const double t = (s_sum[0][tid] + s_sum[1][tid]) + (s_sum[2][tid] + s_sum[3][tid]);
-    const float m = fmaxf(fmaxf(s_max[0][tid], s_max[1][tid]), fmaxf(s_max[2][tid], s_max[3][tid]));
+    double t = s_sum[0][tid];
+    float m = s_max[0][tid];
+#pragma unroll
+    for (int g = 1; g < RQ; ++g) {
+      t += s_sum[g][tid];
+      m = fmaxf(m, s_max[g][tid]);
+    }
     const int64_t o = ((int64_t)bh * args.R + a) * D + tid;
     (which == 0 ? args.Qbar : args.Kbar)[o] = t / (double)n;
     (which == 0 ? args.Qmax : args.Kmax)[o] = (double)m;

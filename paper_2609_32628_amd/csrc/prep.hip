@@ -50,17 +50,17 @@ __global__ __launch_bounds__(256) void prep_vstats_kernel(PrepArgs args) {
   const int cc = tid % CPR, rg = tid / CPR;
   const int t0 = blockIdx.x * kVstatRows;
   const T* X = static_cast<const T*>(args.V) + (int64_t)b * args.sb + (int64_t)h * args.sh + cc * EPC;
-  float x[RPT][EPC];
+  // unconditional loads so that they overlap: rows past the end read the last
+  // token again, which changes no maximum
+  uint4 raw[RPT];
 #pragma unroll
   for (int k = 0; k < RPT; ++k) {
-    const int t = t0 + rg + RG * k;
-    if (t < args.N) {
-      load_chunk(X + (int64_t)t * args.sn, x[k]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) x[k][e] = 0.0f;
-    }
+    const int t = min(t0 + rg + RG * k, args.N - 1);
+    raw[k] = *reinterpret_cast<const uint4*>(X + (int64_t)t * args.sn);
   }
+  float x[RPT][EPC];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) chunk_floats<T>(raw[k], x[k]);
   float m[EPC];
 #pragma unroll
   for (int e = 0; e < EPC; ++e) {
@@ -198,20 +198,32 @@ __global__ __launch_bounds__(256) void prep_qk_kernel(PrepArgs args) {
 
   // group u: fragment row rr = 32 jq + r (slot rr for Q, kappa(jq, r) for K),
   // channels [16 c16, 16 c16 + 16)
+  // token indices first, then the data loads, all unconditional (padding slots
+  // read the last valid row and are zeroed), so the loads overlap
+  constexpr int CPG = 16 / EPC;  // 16-byte chunks per group
+  int tok[UPT];
+#pragma unroll
+  for (int k = 0; k < UPT; ++k) {
+    const int u = tid + 256 * k, rr = u / NG;
+    const int slot = which == 0 ? rr : kappa(rr >> 5, rr & 31);
+    tok[k] = slots[min(slot, n - 1)];
+  }
+  uint4 raw[UPT][CPG];
+#pragma unroll
+  for (int k = 0; k < UPT; ++k) {
+    const int c16 = (tid + 256 * k) % NG;
+    const T* p = X + (int64_t)tok[k] * args.sn + 16 * c16;
+#pragma unroll
+    for (int q = 0; q < CPG; ++q) raw[k][q] = *reinterpret_cast<const uint4*>(p + q * EPC);
+  }
   float x[UPT][16];
   float amax = 0.0f;
 #pragma unroll
   for (int k = 0; k < UPT; ++k) {
-    const int u = tid + 256 * k, c16 = u % NG, rr = u / NG;
+    const int u = tid + 256 * k, rr = u / NG;
     const int slot = which == 0 ? rr : kappa(rr >> 5, rr & 31);
-    if (slot < n) {
-      const T* p = X + (int64_t)slots[slot] * args.sn + 16 * c16;
 #pragma unroll
-      for (int q = 0; q < 16 / EPC; ++q) load_chunk(p + q * EPC, x[k] + q * EPC);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) x[k][e] = 0.0f;
-    }
+    for (int q = 0; q < CPG; ++q) chunk_floats<T>(masked(raw[k][q], lane_mask(slot < n)), x[k] + q * EPC);
 #pragma unroll
     for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(x[k][e]));
   }
@@ -276,14 +288,6 @@ __global__ __launch_bounds__(256) void prep_qk_kernel(PrepArgs args) {
 }
 
 // ---- V ------------------------------------------------------------------------
-// Two channels (2p, 2p+1) of slot s from the LDS tile, as floats.
-__device__ inline float2 tile_pair(const uint16_t* tile, int D, int s, int p) {
-  const uint32_t w = reinterpret_cast<const uint32_t*>(tile + s * D)[p];
-  return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
-}
-__device__ inline float2 tile_pair(const float* tile, int D, int s, int p) {
-  return reinterpret_cast<const float2*>(tile + s * D)[p];
-}
 
 template <int D, typename T>
 __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
@@ -300,11 +304,17 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
   const uint32_t* st = args.stats + (int64_t)bh * (4 + D);
   const int64_t blk = (int64_t)bh * R + a;
 
+  // token indices first, then the data loads, all unconditional (padding slots
+  // read the last valid row and are zeroed), so the loads overlap
+  int tok[LPT];
+#pragma unroll
+  for (int k = 0; k < LPT; ++k) tok[k] = slots[min((tid + 256 * k) / CPR, n - 1)];
   uint4 v[LPT];
 #pragma unroll
   for (int k = 0; k < LPT; ++k) {
     const int ci = tid + 256 * k, s = ci / CPR, cc = ci % CPR;
-    v[k] = s < n ? *reinterpret_cast<const uint4*>(X + (int64_t)slots[s] * args.sn + cc * EPC) : make_uint4(0u, 0u, 0u, 0u);
+    const uint4 x = *reinterpret_cast<const uint4*>(X + (int64_t)tok[k] * args.sn + cc * EPC);
+    v[k] = masked(x, lane_mask(s < n));
   }
 #pragma unroll
   for (int k = 0; k < LPT; ++k) {
