@@ -119,9 +119,15 @@ struct Fp4Group {
   f16x2 s2;
   float y[16];
 };
+// E4M3 value of a in [0, 448]: v_cvt_pk_fp8_f32 rounds to nearest even (the
+// device format tests check it against the format definition on that range)
+// and v_cvt_f32_fp8 returns the exact value.
+__device__ inline float e4m3_round_hw(float a) {
+  return __builtin_amdgcn_cvt_f32_fp8(__builtin_amdgcn_cvt_pk_fp8_f32(a, 0.0f, 0, false), 0);
+}
 __device__ inline void fp4_setup(Fp4Group& G, float gmax, float c, float mn) {
   const float pmax = exp2_fast(__builtin_fmaf(gmax, c, -mn));
-  const float sigma = e4m3_round_mag(fminf(448.0f * pmax, 448.0f));
+  const float sigma = e4m3_round_hw(fminf(448.0f * pmax, 448.0f));
   const bool nz = sigma > 0.0f;
   G.off = (nz ? kLog2_2688 - __builtin_amdgcn_logf(sigma) : 0.0f) - mn;
   G.scale = nz ? sigma * (1.0f / 2688.0f) : 1.0f;

@@ -41,8 +41,8 @@ def probe():
     outs = {k: torch.empty(n, dtype=dt, device="cuda") for k, dt in
             [("e2m1_sw", torch.float32), ("e2m1_hw", torch.float32), ("e2m1_hw_s2", torch.float32),
              ("e2m1_hw_back3", torch.float32), ("e4m3_sw", torch.int32), ("e4m3_hw", torch.int32),
-             ("e4m3_mag_sw", torch.float32)]}
-    order = ["e2m1_sw", "e2m1_hw", "e2m1_hw_s2", "e2m1_hw_back3", "e4m3_sw", "e4m3_hw", "e4m3_mag_sw"]
+             ("e4m3_mag_sw", torch.float32), ("e4m3_mag_hw", torch.float32)]}
+    order = ["e2m1_sw", "e2m1_hw", "e2m1_hw_s2", "e2m1_hw_back3", "e4m3_sw", "e4m3_hw", "e4m3_mag_sw", "e4m3_mag_hw"]
     args = [ctypes.c_void_p(xd.data_ptr()), ctypes.c_int(n)] + [ctypes.c_void_p(outs[k].data_ptr()) for k in order]
     args.append(ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
     assert lib.da2_probe_formats(*args) == 0
@@ -69,6 +69,15 @@ def test_hardware_fp8_conversion_is_rne_in_range(probe):
     got = o["e4m3_hw"][inr].astype(np.uint8)
     bad = np.nonzero(got != want)[0]
     assert bad.size == 0, [(x[inr][i], got[i], want[i]) for i in bad[:10]]
+
+
+def test_hardware_fp8_round_trip_value(probe):
+    """v_cvt_pk_fp8_f32 then v_cvt_f32_fp8 on |x| clamped to 448 (how the
+    attention rounds the NVFP4 weight scales sigma_P) gives the E4M3 value."""
+    x, o = probe
+    want = F.e4m3(np.minimum(np.abs(x), 448.0))
+    bad = np.nonzero(o["e4m3_mag_hw"] != want)[0]
+    assert bad.size == 0, [(x[i], o["e4m3_mag_hw"][i], want[i]) for i in bad[:10]]
 
 
 def test_hardware_fp4_conversion(probe):
