@@ -25,6 +25,8 @@ pytestmark = pytest.mark.gpu
 
 CASES = [configs.TINY, SMALL]
 SMALL_RAGGED = replace(SMALL, name="small-ragged-3x13x21", partition="ragged")
+# fp32 storage at d = 128 (the d = 64 fp32 path is the tiny case)
+SMALL_F32 = replace(SMALL, name="small-f32-3x13x21", dtype="fp32")
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -51,7 +53,7 @@ def _run_gpu(w, Q, K, V, budgets=None, scope=None, odtype=torch.float32):
     return buf, p, O
 
 
-@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED], ids=lambda w: w.name)
+@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED, SMALL_F32], ids=lambda w: w.name)
 def test_draft_map(w):
     log(f"draft_map parity {w.name}")
     Q, K, V = inputs(w)
@@ -121,7 +123,7 @@ def test_rank_assign_injected(scope, budgets16):
     assert np.all(np.diff(cost[order])[same] <= 5 * R * 2 * BH // 8192 + 5)   # longest first within a group
 
 
-@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED], ids=lambda w: w.name)
+@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED, SMALL_F32], ids=lambda w: w.name)
 def test_prep_operands(w):
     log(f"prep_operands parity {w.name}")
     Q, K, V = inputs(w)
@@ -146,7 +148,7 @@ def test_prep_operands(w):
             assert np.array_equal(got[name][bh].view(np.uint32), want[name].view(np.uint32)), (name, bh)
 
 
-@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED], ids=lambda w: w.name)
+@pytest.mark.parametrize("w", CASES + [SMALL_RAGGED, SMALL_F32], ids=lambda w: w.name)
 def test_prep_operands_mxfp4(w):
     """fmt4 = MXFP4: the three MXFP4 sections byte for byte (codes, scale
     words, unused words zero), and the 8-bit sections unchanged."""
@@ -253,7 +255,8 @@ E2E_CASES = CASES + [replace(SMALL, name="small-16bit-15/10/30", num16=15), SMAL
                      replace(SMALL_RAGGED, name="small-ragged-16bit", num16=20, scope="row"),
                      replace(configs.TINY, name="tiny-mxfp4", fmt4="mxfp4"),
                      replace(SMALL, name="small-mxfp4", fmt4="mxfp4"),
-                     replace(SMALL_RAGGED, name="small-ragged-mxfp4-16bit", fmt4="mxfp4", num16=10)]
+                     replace(SMALL_RAGGED, name="small-ragged-mxfp4-16bit", fmt4="mxfp4", num16=10),
+                     SMALL_F32, replace(SMALL_F32, name="small-f32-mxfp4-16bit", fmt4="mxfp4", num16=10)]
 
 
 @pytest.mark.parametrize("w", E2E_CASES, ids=lambda w: w.name)
