@@ -3,7 +3,8 @@
 //   prep_vstats  token-major pass over V of each head: per-channel max|V| and
 //                the head's max|V| (every token is a valid key).
 //   prep_qk      one workgroup per (block, head, Q or K): gathers the block's
-//                64 slots through slot2tok in 16-byte loads (padding = 0);
+//                64 slots through slot2tok in 16-byte loads (unconditional, so
+//                they overlap; padding slots are masked to 0);
 //                each thread owns whole 16-channel groups, so the INT8 block
 //                code and the NVFP4 group code of a group come from registers.
 //   prep_v       one workgroup per (block, head): the V tile is staged in LDS
