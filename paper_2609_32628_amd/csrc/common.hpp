@@ -97,6 +97,17 @@ __device__ inline float2 tile_pair(const float* tile, int D, int s, int p) {
   return reinterpret_cast<const float2*>(tile + s * D)[p];
 }
 
+// ---- INT8 ------------------------------------------------------------------
+// INT8 code of y: round half away from zero, clamped to [-127, 127]. After the
+// clamp, truncating y + copysign(0.5 - 2^-25, y) (one correctly rounded add)
+// rounds half away from zero exactly for every float32 with |y| <= 130 (checked
+// exhaustively against the definition); the clamp commutes with the rounding
+// because its bounds are integers.
+__device__ inline int int8_code(float y) {
+  const float t = fminf(fmaxf(y, -127.0f), 127.0f);
+  return static_cast<int>(t + __builtin_copysignf(0.49999997f, t));
+}
+
 // ---- E4M3 ------------------------------------------------------------------
 // Value of a >= 0 after a round-to-nearest-even cast to E4M3 (saturating).
 // Branch-free: both the subnormal (step 2^-9) and the normal rounding are

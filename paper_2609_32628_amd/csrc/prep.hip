@@ -120,8 +120,7 @@ __device__ inline uint4 int8_codes16(const float* x, float inv) {
     uint32_t packed = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float v = fminf(fmaxf(roundf(__fmul_rn(x[4 * q + e], inv)), -127.0f), 127.0f);
-      packed |= (static_cast<uint32_t>(static_cast<int>(v)) & 0xFFu) << (8 * e);
+      packed |= (static_cast<uint32_t>(int8_code(__fmul_rn(x[4 * q + e], inv))) & 0xFFu) << (8 * e);
     }
     w[q] = packed;
   }

@@ -8,7 +8,7 @@ typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 
 __global__ void fmt_probe_kernel(const float* x, int n, float* e2m1_sw, float* e2m1_hw, float* e2m1_hw_s2,
                                  float* e2m1_hw_back3, uint32_t* e4m3_sw, uint32_t* e4m3_hw, float* e4m3_mag_sw,
-                                 float* e4m3_mag_hw) {
+                                 float* e4m3_mag_hw, int32_t* int8_code) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const float v = x[i];
@@ -29,14 +29,15 @@ __global__ void fmt_probe_kernel(const float* x, int n, float* e2m1_sw, float* e
   e4m3_mag_sw[i] = da2::e4m3_round_mag(fabsf(v));
   // value round trip as the attention's weight scales use it (|v| clamped to 448)
   e4m3_mag_hw[i] = __builtin_amdgcn_cvt_f32_fp8(__builtin_amdgcn_cvt_pk_fp8_f32(fminf(fabsf(v), 448.0f), 0.0f, 0, false), 0);
+  int8_code[i] = da2::int8_code(v);
 }
 
 extern "C" int da2_probe_formats(const float* x, int n, float* e2m1_sw, float* e2m1_hw, float* e2m1_hw_s2,
                                  float* e2m1_hw_back3, uint32_t* e4m3_sw, uint32_t* e4m3_hw, float* e4m3_mag_sw,
-                                 float* e4m3_mag_hw, void* stream) {
+                                 float* e4m3_mag_hw, int32_t* int8_code, void* stream) {
   if (n <= 0 || !x) return -1;
   hipLaunchKernelGGL(fmt_probe_kernel, dim3((n + 255) / 256), dim3(256), 0, (hipStream_t)stream, x, n, e2m1_sw,
-                     e2m1_hw, e2m1_hw_s2, e2m1_hw_back3, e4m3_sw, e4m3_hw, e4m3_mag_sw, e4m3_mag_hw);
+                     e2m1_hw, e2m1_hw_s2, e2m1_hw_back3, e4m3_sw, e4m3_hw, e4m3_mag_sw, e4m3_mag_hw, int8_code);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 

@@ -20,7 +20,9 @@ def _values():
     mids4 = (e4[:-1] + e4[1:]) / 2
     e2 = F.E2M1_VALUES
     mids2 = (e2[:-1] + e2[1:]) / 2
-    base = np.concatenate([e4, mids4, e2, mids2, [448.0, 449.0, 464.0, 470.0, 500.0, 1e6, 6.0, 6.5, 7.0, 100.0]])
+    ints = np.arange(0, 131, dtype=np.float64)
+    base = np.concatenate([e4, mids4, e2, mids2, ints, ints + 0.5,
+                           [448.0, 449.0, 464.0, 470.0, 500.0, 1e6, 6.0, 6.5, 7.0, 100.0]])
     base = base.astype(np.float32)
     up = np.nextafter(base, np.float32(np.inf))
     down = np.nextafter(base, np.float32(0))
@@ -41,8 +43,9 @@ def probe():
     outs = {k: torch.empty(n, dtype=dt, device="cuda") for k, dt in
             [("e2m1_sw", torch.float32), ("e2m1_hw", torch.float32), ("e2m1_hw_s2", torch.float32),
              ("e2m1_hw_back3", torch.float32), ("e4m3_sw", torch.int32), ("e4m3_hw", torch.int32),
-             ("e4m3_mag_sw", torch.float32), ("e4m3_mag_hw", torch.float32)]}
-    order = ["e2m1_sw", "e2m1_hw", "e2m1_hw_s2", "e2m1_hw_back3", "e4m3_sw", "e4m3_hw", "e4m3_mag_sw", "e4m3_mag_hw"]
+             ("e4m3_mag_sw", torch.float32), ("e4m3_mag_hw", torch.float32), ("int8_code", torch.int32)]}
+    order = ["e2m1_sw", "e2m1_hw", "e2m1_hw_s2", "e2m1_hw_back3", "e4m3_sw", "e4m3_hw", "e4m3_mag_sw", "e4m3_mag_hw",
+             "int8_code"]
     args = [ctypes.c_void_p(xd.data_ptr()), ctypes.c_int(n)] + [ctypes.c_void_p(outs[k].data_ptr()) for k in order]
     args.append(ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
     assert lib.da2_probe_formats(*args) == 0
@@ -69,6 +72,16 @@ def test_hardware_fp8_conversion_is_rne_in_range(probe):
     got = o["e4m3_hw"][inr].astype(np.uint8)
     bad = np.nonzero(got != want)[0]
     assert bad.size == 0, [(x[inr][i], got[i], want[i]) for i in bad[:10]]
+
+
+def test_int8_code(probe):
+    """The INT8 encoder's rounding (operand preparation): round half away from
+    zero, clamped to [-127, 127], on every integer +- 0.5 tie up to 130, their
+    float32 neighbours and the rest of the probe set."""
+    x, o = probe
+    want = np.clip(F.half_away(x.astype(np.float32)), -127, 127)
+    bad = np.nonzero(o["int8_code"] != want)[0]
+    assert bad.size == 0, [(x[i], o["int8_code"][i], want[i]) for i in bad[:10]]
 
 
 def test_hardware_fp8_round_trip_value(probe):
