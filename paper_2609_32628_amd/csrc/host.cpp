@@ -68,7 +68,8 @@ void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
   s->ws_draft_bytes = 4 * align_up(8 * d.BH * d.R * d.d) + 2 * align_up(8 * d.BH * d.R * d.R);
   int64_t thr = scope == DA2_SCOPE_ROW ? 8 * da2::kCuts * d.BH * d.R : 8 * da2::kCuts * d.BH;
   s->ws_rank_bytes = align_up(4 * d.BH * da2::kCuts * 2048) + align_up(thr) + align_up(8 * da2::kCuts * d.BH) +
-                     align_up(8 * da2::kCuts * d.BH) + align_up(4 * d.BH * d.R);
+                     align_up(8 * da2::kCuts * d.BH) + align_up(4 * d.BH * d.R) +
+                     align_up(8 * d.BH * da2::kCuts * da2::kRankCand) + align_up(4 * d.BH * da2::kCuts);
   s->ws_prep_bytes = 0;
 }
 
@@ -353,6 +354,10 @@ int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int
   a.kleft = reinterpret_cast<int64_t*>(w + o);
   o += align_up(8 * da2::kCuts * d.BH);
   a.cost = reinterpret_cast<int32_t*>(w + o);
+  o += align_up(4 * d.BH * d.R);
+  a.cand = reinterpret_cast<uint64_t*>(w + o);
+  o += align_up(8 * d.BH * da2::kCuts * da2::kRankCand);
+  a.ccount = reinterpret_cast<uint32_t*>(w + o);
   return hip_status(da2::launch_rank(a, static_cast<hipStream_t>(stream)));
 }
 

@@ -22,6 +22,8 @@ struct DraftArgs {
 
 constexpr int kCuts = 3;  // rank cut points: T16, T16+T8, T16+T8+T4
 
+constexpr int kRankCand = 2048;  // candidate keys per (head, cut) the ranking resolves directly
+
 struct RankArgs {
   const float* A;
   int B, H, R;
@@ -37,6 +39,8 @@ struct RankArgs {
   uint64_t* thr;           // head: [BH][kCuts]; row: [BH*R][kCuts]
   uint64_t* prefix;        // [BH][kCuts]
   int64_t* kleft;          // [BH][kCuts]
+  uint64_t* cand;          // [BH][kCuts][kRankCand] keys collected in the third histogram pass
+  uint32_t* ccount;        // [BH][kCuts] number collected (> kRankCand: too many, not used)
   int32_t* cost;           // [BH*R]
 };
 

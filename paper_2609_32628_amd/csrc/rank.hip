@@ -11,7 +11,11 @@
 // Head scope finds the three threshold keys with a 5-pass most-significant-digit
 // radix select (11,11,11,11,10 bits) over all R^2 keys of a head: a histogram
 // kernel spread over many workgroups, then a one-workgroup scan per head that
-// fixes the next digit. Row scope sorts each row's R keys in LDS (bitonic).
+// fixes the next digit. The third pass also collects the keys that match a
+// cut's 22-bit prefix (the threshold is one of them); when there are at most
+// kRankCand of them, its scan sorts them and reads the threshold key directly,
+// and the last two passes skip that cut. Row scope sorts each row's R keys in
+// LDS (bitonic).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -23,6 +27,8 @@ __constant__ int kShift[kPasses] = {43, 32, 21, 10, 0};
 __constant__ int kWidth[kPasses] = {11, 11, 11, 11, 10};
 constexpr int kHistChunk = 8192;
 constexpr uint64_t kNone = ~0ull;
+constexpr int kCollectPass = 2;   // the pass that collects candidate keys
+constexpr int kLocalCand = 256;   // candidates one histogram workgroup stages per cut
 
 __device__ inline uint64_t rank_key(float a, uint32_t idx) {
   if (a == 0.0f) a = 0.0f;  // -0 ranks like +0
@@ -38,6 +44,7 @@ __global__ void rank_init_kernel(RankArgs args) {
     const int t = threadIdx.x;
     args.prefix[bh * kCuts + t] = 0ull;
     args.kleft[bh * kCuts + t] = args.cut[t];
+    args.ccount[bh * kCuts + t] = 0u;
   }
 }
 
@@ -55,7 +62,10 @@ __device__ inline void hist_slots(const RankArgs& args, int bh, int hi, int (&sl
 
 __global__ __launch_bounds__(256) void rank_hist_kernel(RankArgs args, int pass) {
   __shared__ uint32_t lh[kCuts][kBins];
+  __shared__ uint64_t lc[kCuts][kLocalCand];  // staged candidates (collecting pass)
+  __shared__ uint32_t lcnt[kCuts], lbase[kCuts];
   const int bh = blockIdx.y;
+  const bool collect = pass == kCollectPass;
   const int64_t M = (int64_t)args.R * args.R;
   const int sh = kShift[pass], hi = sh + kWidth[pass];
   const uint64_t mask = (1ull << kWidth[pass]) - 1ull;
@@ -68,6 +78,7 @@ __global__ __launch_bounds__(256) void rank_hist_kernel(RankArgs args, int pass)
     own[t] = slot[t] == t;
     any = any || own[t];
   }
+  if (threadIdx.x < kCuts) lcnt[threadIdx.x] = 0u;
   __syncthreads();
   if (any) {
     const float* A = args.A + (int64_t)bh * M;
@@ -86,7 +97,13 @@ __global__ __launch_bounds__(256) void rank_hist_kernel(RankArgs args, int pass)
         const uint32_t dig = static_cast<uint32_t>((key >> sh) & mask);
 #pragma unroll
         for (int t = 0; t < kCuts; ++t)
-          if (own[t] && (key >> hi) == pre[t]) atomicAdd(&lh[t][dig], 1u);
+          if (own[t] && (key >> hi) == pre[t]) {
+            atomicAdd(&lh[t][dig], 1u);
+            if (collect) {
+              const uint32_t pos = atomicAdd(&lcnt[t], 1u);
+              if (pos < kLocalCand) lc[t][pos] = key;
+            }
+          }
       }
     }
   }
@@ -97,6 +114,46 @@ __global__ __launch_bounds__(256) void rank_hist_kernel(RankArgs args, int pass)
     for (int i = threadIdx.x; i < kBins; i += 256) {
       const uint32_t v = lh[t][i];
       if (v) atomicAdd(gh + t * kBins + i, v);
+    }
+  }
+  if (collect) {
+    // reserve room in the head's candidate list; a workgroup with more than
+    // kLocalCand candidates marks the list as too long (count > kRankCand)
+    if (threadIdx.x < kCuts) {
+      const int t = threadIdx.x;
+      const uint32_t c = lcnt[t];
+      uint32_t base = kRankCand;
+      if (own[t] && c > 0)
+        base = atomicAdd(args.ccount + bh * kCuts + t, c <= (uint32_t)kLocalCand ? c : (uint32_t)kRankCand + 1u);
+      lbase[t] = base;
+    }
+    __syncthreads();
+    for (int t = 0; t < kCuts; ++t) {
+      const uint32_t c = lcnt[t], base = lbase[t];
+      if (!own[t] || c == 0 || c > (uint32_t)kLocalCand || base + c > (uint32_t)kRankCand) continue;  // uniform
+      uint64_t* dst = args.cand + ((int64_t)bh * kCuts + t) * kRankCand + base;
+      for (uint32_t i = threadIdx.x; i < c; i += 256) dst[i] = lc[t][i];
+    }
+  }
+}
+
+// Descending bitonic sort of n (a power of two, <= kRankCand) keys in LDS by a
+// 256-thread block.
+__device__ inline void block_sort_desc(uint64_t* sk, int n) {
+  for (int k = 2; k <= n; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < n; i += 256) {
+        const int l = i ^ j;
+        if (l > i) {
+          const bool desc = (i & k) == 0;
+          const uint64_t x = sk[i], y = sk[l];
+          if (desc ? (x < y) : (x > y)) {
+            sk[i] = y;
+            sk[l] = x;
+          }
+        }
+      }
+      __syncthreads();
     }
   }
 }
@@ -120,6 +177,7 @@ __device__ inline uint32_t block_exscan_256(uint32_t v, uint32_t* sh, uint32_t* 
 
 __global__ __launch_bounds__(256) void rank_scan_kernel(RankArgs args, int pass) {
   __shared__ uint32_t sh[4];
+  __shared__ uint64_t sk[kRankCand];
   const int bh = blockIdx.x;
   const int s = kShift[pass];
   uint32_t* gh = args.hist + (int64_t)bh * kCuts * kBins;
@@ -127,9 +185,31 @@ __global__ __launch_bounds__(256) void rank_scan_kernel(RankArgs args, int pass)
   int slot[kCuts];
   uint64_t pre[kCuts];
   hist_slots(args, bh, s + kWidth[pass], slot, pre);
+  uint32_t ncand[kCuts];
+  for (int t = 0; t < kCuts; ++t)
+    ncand[t] = pass == kCollectPass && slot[t] >= 0 ? args.ccount[bh * kCuts + slot[t]] : (uint32_t)kRankCand + 1u;
+  __syncthreads();  // every thread has read the counts and prefixes before any changes
   for (int t = 0; t < kCuts; ++t) {
     const int64_t k = args.kleft[bh * kCuts + t];
     if (k <= 0) continue;  // uniform across the block
+    if (ncand[t] >= 1u && ncand[t] <= (uint32_t)kRankCand && k <= (int64_t)ncand[t]) {
+      // the collected keys are exactly those with this cut's prefix, and the
+      // threshold is the k-th largest of them (1 <= k <= ncand always holds
+      // here; anything else takes the histogram path below)
+      const int n = (int)ncand[t];
+      int np = 1;
+      while (np < n) np <<= 1;
+      const uint64_t* src = args.cand + ((int64_t)bh * kCuts + slot[t]) * kRankCand;
+      for (int i = threadIdx.x; i < np; i += 256) sk[i] = i < n ? src[i] : 0ull;
+      __syncthreads();
+      block_sort_desc(sk, np);
+      if (threadIdx.x == 0) {
+        args.prefix[bh * kCuts + t] = sk[k - 1];
+        args.kleft[bh * kCuts + t] = 0;
+      }
+      __syncthreads();
+      continue;
+    }
     // thread i owns bins [2047-8i-7, 2047-8i], visited from the top
     uint32_t c[8], local = 0;
     for (int q = 0; q < 8; ++q) {
