@@ -299,7 +299,15 @@ __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
   const int a = blockIdx.x, bh = blockIdx.y, R = args.R;
   const int64_t row = (int64_t)bh * R + a;
   const float* A = args.A + row * R;
-  for (int b = threadIdx.x; b < R; b += 256) srow[b] = A[b];
+  // eight loads in flight per thread (indices past the row read its last entry)
+  for (int b0 = threadIdx.x; b0 < R; b0 += 256 * 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = A[min(b0 + 256 * u, R - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (b0 + 256 * u < R) srow[b0 + 256 * u] = v[u];
+  }
   __syncthreads();
   const bool head = args.scope == DA2_SCOPE_HEAD;
   const uint64_t* thr = head ? args.thr + (int64_t)bh * kCuts : args.thr + row * kCuts;
