@@ -96,6 +96,11 @@ __device__ inline float2 tile_pair(const uint16_t* tile, int D, int s, int p) {
 __device__ inline float2 tile_pair(const float* tile, int D, int s, int p) {
   return reinterpret_cast<const float2*>(tile + s * D)[p];
 }
+// Channel c of row s of a [rows][D] tile in LDS, as a float.
+__device__ inline float tile_value(const uint16_t* tile, int D, int s, int c) {
+  return __uint_as_float(static_cast<uint32_t>(tile[s * D + c]) << 16);
+}
+__device__ inline float tile_value(const float* tile, int D, int s, int c) { return tile[s * D + c]; }
 
 // ---- INT8 ------------------------------------------------------------------
 // INT8 code of y: round half away from zero, clamped to [-127, 127]. After the

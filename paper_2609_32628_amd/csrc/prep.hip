@@ -8,8 +8,9 @@
 //                each thread owns whole 16-channel groups, so the INT8 block
 //                code and the NVFP4 group code of a group come from registers.
 //   prep_v       one workgroup per (block, head): the V tile is staged in LDS
-//                and read transposed, each thread owning one channel pair and
-//                one 16-slot group (the NVFP4 group of V runs along slots).
+//                and read transposed, each thread owning channels c and c + d/2
+//                and one 16-slot group (the NVFP4 group of V runs along
+//                slots), so each store fills consecutive fragment lanes.
 // Every encoding is written in the MFMA fragment order of the attention kernel
 // (16-byte chunks, one per lane of a fragment):
 //   INT8 Q, K with per-block scales, E4M3 V with per-channel scales,
@@ -323,22 +324,23 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
   }
   __syncthreads();
 
-  // unit: channel pair p, 16-slot group sg
+  // unit: channels p and p + D/2, 16-slot group sg (consecutive threads own
+  // consecutive channels, so each store instruction below fills consecutive
+  // 16-byte lanes of a fragment)
   const int p = tid % (D / 2), sg = tid / (D / 2);
   if (sg < 4) {
     float x0[16], x1[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const float2 f = tile_pair(tile, D, 16 * sg + i, p);
-      x0[i] = f.x;
-      x1[i] = f.y;
+      x0[i] = tile_value(tile, D, 16 * sg + i, p);
+      x1[i] = tile_value(tile, D, 16 * sg + i, p + D / 2);
     }
     const float gV = nvfp4_scale_global(st[2]);
     const float sixg = __fmul_rn(6.0f, gV);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const float* xc = q == 0 ? x0 : x1;
-      const int c = 2 * p + q;
+      const int c = p + q * (D / 2);
       const int lane = (c & 31) + 32 * (sg & 1), t = c >> 5;
       // E4M3, per-channel scale: chunk [t][h = sg/2][lane][16]
       const float dlt = __fdiv_rn(__uint_as_float(st[4 + c]), 2.25f);
@@ -369,7 +371,7 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
       }
     }
   }
-  // MXFP4 along slots: unit = channel pair p, 32-slot block hb; the block's
+  // MXFP4 along slots: unit = channels p and p + D/2, 32-slot block hb; the block's
   // 32 codes fill the 16 bytes of lane c%32 + 32 hb in data fragment t = c/32.
   constexpr int NT = D / 32;
   if (args.fmt4 == DA2_FMT4_MXFP4 && tid < D) {
@@ -377,15 +379,14 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
     float x0[32], x1[32];
 #pragma unroll
     for (int i = 0; i < 32; ++i) {
-      const float2 f = tile_pair(tile, D, 32 * hb + i, p);
-      x0[i] = f.x;
-      x1[i] = f.y;
+      x0[i] = tile_value(tile, D, 32 * hb + i, p);
+      x1[i] = tile_value(tile, D, 32 * hb + i, p + D / 2);
     }
     uint8_t* base = args.V4mx + blk * (int64_t)mx_block_bytes(D);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       float* xc = q == 0 ? x0 : x1;
-      const int c = 2 * p + q, t = c >> 5, ml = (c & 31) + 32 * hb;
+      const int c = p + q * (D / 2), t = c >> 5, ml = (c & 31) + 32 * hb;
       float m = 0.0f;
 #pragma unroll
       for (int i = 0; i < 32; ++i) m = fmaxf(m, fabsf(xc[i]));
