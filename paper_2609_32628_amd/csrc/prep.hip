@@ -38,37 +38,42 @@ __global__ void zero_vstats_kernel(uint32_t* stats, int d) {
 }
 
 // ---- V statistics -----------------------------------------------------------
-constexpr int kVstatRows = 256;  // tokens per workgroup
+constexpr int kVstatRows = 1024;  // tokens per workgroup (one atomic max per channel per workgroup)
 
 template <int D, typename T>
 __global__ __launch_bounds__(256) void prep_vstats_kernel(PrepArgs args) {
   constexpr int EPC = 16 / sizeof(T);   // elements per 16-byte load
   constexpr int CPR = D / EPC;          // loads per token row
   constexpr int RG = 256 / CPR;         // row groups
-  constexpr int RPT = kVstatRows / RG;  // rows per thread
+  constexpr int RPR = 16;               // rows per thread per round (loads in flight)
+  constexpr int ROUNDS = kVstatRows / (RG * RPR);
+  static_assert(ROUNDS * RG * RPR == kVstatRows, "whole rounds");
   __shared__ float s_max[4][D];
   __shared__ float s_all[4];
   const int bh = blockIdx.y, b = bh / args.H, h = bh % args.H, tid = threadIdx.x;
   const int cc = tid % CPR, rg = tid / CPR;
   const int t0 = blockIdx.x * kVstatRows;
   const T* X = static_cast<const T*>(args.V) + (int64_t)b * args.sb + (int64_t)h * args.sh + cc * EPC;
-  // unconditional loads so that they overlap: rows past the end read the last
-  // token again, which changes no maximum
-  uint4 raw[RPT];
-#pragma unroll
-  for (int k = 0; k < RPT; ++k) {
-    const int t = min(t0 + rg + RG * k, args.N - 1);
-    raw[k] = *reinterpret_cast<const uint4*>(X + (int64_t)t * args.sn);
-  }
-  float x[RPT][EPC];
-#pragma unroll
-  for (int k = 0; k < RPT; ++k) chunk_floats<T>(raw[k], x[k]);
   float m[EPC];
 #pragma unroll
-  for (int e = 0; e < EPC; ++e) {
-    m[e] = fabsf(x[0][e]);
+  for (int e = 0; e < EPC; ++e) m[e] = 0.0f;
+#pragma unroll 1
+  for (int rd = 0; rd < ROUNDS; ++rd) {
+    // unconditional loads so that they overlap: rows past the end read the
+    // last token again, which changes no maximum
+    uint4 raw[RPR];
 #pragma unroll
-    for (int k = 1; k < RPT; ++k) m[e] = fmaxf(m[e], fabsf(x[k][e]));
+    for (int k = 0; k < RPR; ++k) {
+      const int t = min(t0 + rd * RG * RPR + rg + RG * k, args.N - 1);
+      raw[k] = *reinterpret_cast<const uint4*>(X + (int64_t)t * args.sn);
+    }
+#pragma unroll
+    for (int k = 0; k < RPR; ++k) {
+      float x[EPC];
+      chunk_floats<T>(raw[k], x);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) m[e] = fmaxf(m[e], fabsf(x[e]));
+    }
   }
   // lanes with the same chunk column sit CPR apart in a wave
 #pragma unroll
