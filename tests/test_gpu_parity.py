@@ -456,6 +456,25 @@ def test_bf16_output_and_determinism():
     assert torch.equal(O32.to(torch.bfloat16), O16a)
 
 
+@pytest.mark.parametrize("w", [SMALL, configs.TINY], ids=lambda w: w.name)
+def test_token_major_strided_tensors(w):
+    """Q, K, V and O passed as [B, H, N, d] views of token-major [B, N, H, d]
+    storage (the layout a fused QKV projection writes), through the tensor
+    descriptor's strides: the same draft map, classes and output, bit for bit,
+    as contiguous tensors."""
+    Q, K, V = inputs(w)
+    buf_c, p, O_c = _run_gpu(w, Q, K, V)
+    dev = [to_device(np.ascontiguousarray(X.transpose(0, 2, 1, 3)), w).transpose(1, 2) for X in (Q, K, V)]
+    assert not dev[0].is_contiguous() and dev[0].shape == (w.B, w.H, w.N, w.d)
+    buf = api.alloc(p, w.scope)
+    O_store = torch.full((w.B, w.N, w.H, w.d), float("nan"), dtype=torch.float32, device="cuda")
+    O = O_store.transpose(1, 2)
+    api.attention(*dev, buf, w.lam, w.budgets, O, num16=w.num16, fmt4=w.fmt4)
+    torch.cuda.synchronize()
+    assert torch.equal(buf.A, buf_c.A) and torch.equal(buf.cls, buf_c.cls)
+    assert torch.equal(O.contiguous(), O_c)
+
+
 def test_all_skipped_rows_are_zero():
     w = SMALL
     Q, K, V = inputs(w)
