@@ -211,11 +211,14 @@ __global__ __launch_bounds__(256) void draft_softmax_reg_kernel(DraftArgs args) 
   z1 = wave_sum_f64(z1);
   z2 = wave_sum_f64(z2);
   const double lam = args.lambda;
+  // both normalizations and the mixing weights folded into one factor per
+  // branch (float64; A is rounded once, to float32, at the end)
+  const double r1 = (1.0 - lam) / z1, r2 = lam / z2;
   float* out = args.A + row * R;
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) {
     const int i = lane + 64 * k;
-    if (i < R) out[i] = (float)((1.0 - lam) * (e1[k] / z1) + lam * (e2[k] / z2));
+    if (i < R) out[i] = (float)(e1[k] * r1 + e2[k] * r2);
   }
 }
 
@@ -240,11 +243,9 @@ __global__ __launch_bounds__(256) void draft_softmax_kernel(DraftArgs args) {
   z1 = wave_sum_f64(z1);
   z2 = wave_sum_f64(z2);
   const double lam = args.lambda;
+  const double r1 = (1.0 - lam) / z1, r2 = lam / z2;
   float* out = args.A + row * R;
-  for (int i = lane; i < R; i += 64) {
-    const double p1 = exp(s1[i] - m1) / z1, p2 = exp(s2[i] - m2) / z2;
-    out[i] = (float)((1.0 - lam) * p1 + lam * p2);
-  }
+  for (int i = lane; i < R; i += 64) out[i] = (float)(exp(s1[i] - m1) * r1 + exp(s2[i] - m2) * r2);
 }
 
 hipError_t launch_draft(const DraftArgs& args, hipStream_t stream) {
