@@ -269,44 +269,53 @@ __global__ __launch_bounds__(256) void rank_row_select_kernel(RankArgs args, int
   }
 }
 
-// Exclusive prefix sum of 64-bit values over a 256-thread block.
-__device__ inline uint64_t block_exscan_256_u64(uint64_t v, uint64_t* sh, uint64_t* total) {
+// Exclusive prefix sum of 64-bit values over an NT-thread block (NT = 64: one
+// wave, no LDS; NT = 256: four waves through LDS).
+template <int NT>
+__device__ inline uint64_t block_exscan_u64(uint64_t v, uint64_t* sh, uint64_t* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   uint64_t x = v;
   for (int o = 1; o < 64; o <<= 1) {
     const uint64_t y = __shfl_up(x, o, 64);
     if (lane >= o) x += y;
   }
-  if (lane == 63) sh[w] = x;
-  __syncthreads();
-  uint64_t base = 0;
-  for (int q = 0; q < w; ++q) base += sh[q];
-  *total = sh[0] + sh[1] + sh[2] + sh[3];
-  __syncthreads();
-  return base + x - v;
+  if constexpr (NT == 64) {
+    *total = __shfl(x, 63, 64);
+    return x - v;
+  } else {
+    if (lane == 63) sh[w] = x;
+    __syncthreads();
+    uint64_t base = 0;
+    for (int q = 0; q < w; ++q) base += sh[q];
+    *total = sh[0] + sh[1] + sh[2] + sh[3];
+    __syncthreads();
+    return base + x - v;
+  }
 }
 
 // Classes, ascending per-row lists (4-bit, then 8-bit, then 16-bit: the phase
-// order of the attention), counts and row cost. The row's scores are staged in
-// LDS (R floats, dynamic) with coalesced loads; thread i then owns the
-// contiguous run of key blocks [i E, (i + 1) E), E = ceil(R / 256): it
-// classifies its run, one block-wide scan of the packed per-class counts (21
+// order of the attention), counts and row cost; one NT-thread workgroup per
+// row (NT = 64 for rows of up to 1024 blocks, 256 beyond). The row's scores are
+// staged in LDS (R floats, dynamic) with coalesced loads; thread i then owns
+// the contiguous run of key blocks [i E, (i + 1) E), E = ceil(R / NT): it
+// classifies its run, a block-wide scan of the packed per-class counts (21
 // bits each) gives every class's write offset, and a second walk over the run
 // writes the lists.
-__global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
+template <int NT>
+__global__ __launch_bounds__(NT) void rank_classify_kernel(RankArgs args) {
   extern __shared__ float srow[];
   __shared__ uint64_t sh[4];
-  const int a = blockIdx.x, bh = blockIdx.y, R = args.R;
+  const int a = blockIdx.x, bh = blockIdx.y, R = args.R, tid = threadIdx.x;
   const int64_t row = (int64_t)bh * R + a;
   const float* A = args.A + row * R;
   // eight loads in flight per thread (indices past the row read its last entry)
-  for (int b0 = threadIdx.x; b0 < R; b0 += 256 * 8) {
+  for (int b0 = tid; b0 < R; b0 += NT * 8) {
     float v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = A[min(b0 + 256 * u, R - 1)];
+    for (int u = 0; u < 8; ++u) v[u] = A[min(b0 + NT * u, R - 1)];
 #pragma unroll
     for (int u = 0; u < 8; ++u)
-      if (b0 + 256 * u < R) srow[b0 + 256 * u] = v[u];
+      if (b0 + NT * u < R) srow[b0 + NT * u] = v[u];
   }
   __syncthreads();
   const bool head = args.scope == DA2_SCOPE_HEAD;
@@ -324,8 +333,8 @@ __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
   auto field = [](int c) -> uint64_t {
     return c == 4 ? 1ull : (c == 8 ? (1ull << kF) : (c == 16 ? (1ull << (2 * kF)) : 0ull));
   };
-  const int E = (R + 255) / 256;
-  const int b0 = min(R, static_cast<int>(threadIdx.x) * E), b1 = min(R, b0 + E);
+  const int E = (R + NT - 1) / NT;
+  const int b0 = min(R, tid * E), b1 = min(R, b0 + E);
   uint64_t cnt = 0;
   for (int b = b0; b < b1; ++b) {
     const int c = class_of(b);
@@ -333,7 +342,7 @@ __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
     cnt += field(c);
   }
   uint64_t tot;
-  const uint64_t before = block_exscan_256_u64(cnt, sh, &tot);
+  const uint64_t before = block_exscan_u64<NT>(cnt, sh, &tot);
   const uint32_t n4 = static_cast<uint32_t>(tot & kM), n8 = static_cast<uint32_t>((tot >> kF) & kM),
                  n16 = static_cast<uint32_t>((tot >> (2 * kF)) & kM);
   uint32_t p4 = static_cast<uint32_t>(before & kM);
@@ -348,7 +357,7 @@ __global__ __launch_bounds__(256) void rank_classify_kernel(RankArgs args) {
     else if (c == 16)
       keys[p16++] = static_cast<uint16_t>(b);
   }
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     args.counts[row * 4 + 0] = n4;
     args.counts[row * 4 + 1] = n8;
     args.counts[row * 4 + 2] = n16;
@@ -428,7 +437,10 @@ hipError_t launch_rank(const RankArgs& args, hipStream_t stream) {
     while (P < args.R) P <<= 1;
     hipLaunchKernelGGL(rank_row_select_kernel, dim3(args.R, BH), dim3(256), P * sizeof(uint64_t), stream, args, P);
   }
-  hipLaunchKernelGGL(rank_classify_kernel, dim3(args.R, BH), dim3(256), args.R * sizeof(float), stream, args);
+  if (args.R <= 1024)
+    hipLaunchKernelGGL(rank_classify_kernel<64>, dim3(args.R, BH), dim3(64), args.R * sizeof(float), stream, args);
+  else
+    hipLaunchKernelGGL(rank_classify_kernel<256>, dim3(args.R, BH), dim3(256), args.R * sizeof(float), stream, args);
   hipLaunchKernelGGL(rank_order_kernel, dim3(1), dim3(1024), 0, stream, args);
   return hipGetLastError();
 }
