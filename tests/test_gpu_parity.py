@@ -446,6 +446,25 @@ def test_long_layer_sampled_rows():
     _full_size_sampled(configs.LONG, heads=(17,), n_rows=12, seed=5)
 
 
+def test_mid_layer_16bit_share_sampled_rows():
+    """Mid layer with all three paths: 10% 16-bit, 20% 8-bit, 30% 4-bit."""
+    w = replace(configs.MID, name="mid-16bit-10/20/30", num16=10, budgets=(20, 30, 100))
+    _full_size_sampled(w, heads=(2,), n_rows=12, seed=8)
+
+
+def test_wide_layer_mxfp4_sampled_rows():
+    """Wide layer (1% key outliers x8) with the MXFP4 4-bit encoding."""
+    _full_size_sampled(replace(configs.WIDE, fmt4="mxfp4"), heads=(23,), n_rows=12, seed=9)
+
+
+def test_sweep_workload_ragged_sampled_rows():
+    """The operator sweep's workload at full size: 56 heads, 31x42x84 =
+    109,368 tokens on the ragged partition (R = 1736 regions of 63 tokens),
+    10% 8-bit, 30% NVFP4, 60% skipped."""
+    w = replace(configs.FIG4, name="fig4-10/30/60", budgets=(10, 30, 100))
+    _full_size_sampled(w, heads=(31,), n_rows=12, seed=10)
+
+
 def test_bf16_output_and_determinism():
     w = SMALL
     Q, K, V = inputs(w)
