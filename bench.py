@@ -346,9 +346,10 @@ def main():
     n_a = buf.layout[:buf.sizes["R"]].to(torch.float64)
     kept = (buf.cls.view(w.B * w.H, buf.sizes["R"], buf.sizes["R"]) != 0).to(torch.float64)
     valid_flops = float(4.0 * w.d * (kept * n_a[None, :, None] * n_a[None, None, :]).sum().item())
-    # transcendental-issue floor: 64 x 64 exponentials per retained tile at the
-    # quarter-rate transcendental issue (256 CUs x 4 SIMDs x 16 lanes / 4 per clock, 2.4 GHz)
-    exp_floor_ms = (n8 + n4 + n16) * 4096 / (256 * 4 * 16 / 4 * 2.4e9) * 1e3
+    # transcendental-issue floor: 64 x 64 exponentials per retained tile at one
+    # v_exp_f32 wave instruction per 8 clocks per SIMD (the half rate measured
+    # on gfx950 with independent chains), 256 CUs x 4 SIMDs x 64 lanes / 8 at 2.4 GHz
+    exp_floor_ms = (n8 + n4 + n16) * 4096 / (256 * 4 * 64 / 8 * 2.4e9) * 1e3
     t_attn = stage_ms["mixed_attn"] * 1e-3
     achieved = (F8 + F4 + F16) / t_attn
     mx = args.fmt4 == "mxfp4"
