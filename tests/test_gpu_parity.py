@@ -452,6 +452,14 @@ def test_mid_layer_16bit_share_sampled_rows():
     _full_size_sampled(w, heads=(2,), n_rows=12, seed=8)
 
 
+def test_mid_layer_d64_sampled_rows():
+    """The d = 64 kernels at full size: the mid layer's shape (12 heads, 32,760
+    tokens) with 64-channel heads, NVFP4 and MXFP4."""
+    for fmt4, head in (("nvfp4", 6), ("mxfp4", 9)):
+        w = replace(configs.MID, name=f"mid-d64-{fmt4}", d=64, fmt4=fmt4)
+        _full_size_sampled(w, heads=(head,), n_rows=10, seed=11)
+
+
 def test_wide_layer_mxfp4_sampled_rows():
     """Wide layer (1% key outliers x8) with the MXFP4 4-bit encoding."""
     _full_size_sampled(replace(configs.WIDE, fmt4="mxfp4"), heads=(23,), n_rows=12, seed=9)
