@@ -322,6 +322,10 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
     const uint4 x = *reinterpret_cast<const uint4*>(X + (int64_t)tok[k] * args.sn + cc * EPC);
     v[k] = masked(x, lane_mask(s < n));
   }
+  // this thread's statistics (the head's NVFP4 amax and the amax of channels
+  // p and p + D/2), loaded beside the tile rather than after the barrier
+  const int p = tid % (D / 2), sg = tid / (D / 2);
+  const uint32_t st_g = st[2], st_c0 = st[4 + p], st_c1 = st[4 + p + D / 2];
 #pragma unroll
   for (int k = 0; k < LPT; ++k) {
     const int ci = tid + 256 * k;
@@ -332,7 +336,6 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
   // unit: channels p and p + D/2, 16-slot group sg (consecutive threads own
   // consecutive channels, so each store instruction below fills consecutive
   // 16-byte lanes of a fragment)
-  const int p = tid % (D / 2), sg = tid / (D / 2);
   if (sg < 4) {
     float x0[16], x1[16];
 #pragma unroll
@@ -340,7 +343,7 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
       x0[i] = tile_value(tile, D, 16 * sg + i, p);
       x1[i] = tile_value(tile, D, 16 * sg + i, p + D / 2);
     }
-    const float gV = nvfp4_scale_global(st[2]);
+    const float gV = nvfp4_scale_global(st_g);
     const float sixg = __fmul_rn(6.0f, gV);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -348,7 +351,7 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
       const int c = p + q * (D / 2);
       const int lane = (c & 31) + 32 * (sg & 1), t = c >> 5;
       // E4M3, per-channel scale: chunk [t][h = sg/2][lane][16]
-      const float dlt = __fdiv_rn(__uint_as_float(st[4 + c]), 2.25f);
+      const float dlt = __fdiv_rn(__uint_as_float(q == 0 ? st_c0 : st_c1), 2.25f);
       uint4 code = make_uint4(0u, 0u, 0u, 0u);
       if (dlt != 0.0f) {
         const float inv = __fdiv_rn(1.0f, dlt);
