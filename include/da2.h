@@ -144,8 +144,10 @@ int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const 
                       int64_t ws_bytes, void* stream);
 
 /* Offsets (bytes) inside ws_draft of: [0] Qbar, [1] Qmax, [2] Kbar, [3] Kmax
- * (float64 [B,H,R,d] each), [4] S_avg, [5] S_max (float64 [B,H,R,R] logits). */
-int32_t da2_ws_draft_offsets(const da2_problem* p, int64_t* offsets6);
+ * (float64 [B,H,R,d] each), [4] S_avg, [5] S_max (float64 [B,H,R,R] logits),
+ * [6] the per-block max|Q| and max|K| (float32 [2][B*H][R]) that are reduced
+ * into stats entries 0 and 1. */
+int32_t da2_ws_draft_offsets(const da2_problem* p, int64_t* offsets7);
 
 /* Shared ranking (Algorithm 1; routing appendix). Quotas from budgets
  * num16/den, num8/den and num4/den over M = R*R pairs per head

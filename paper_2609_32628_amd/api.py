@@ -64,7 +64,7 @@ def _offsets(fn, p, n):
 
 
 def da2_ws_draft_offsets(p):
-    return _offsets("da2_ws_draft_offsets", p, 6)
+    return _offsets("da2_ws_draft_offsets", p, 7)
 
 
 def da2_lists_offsets(p):

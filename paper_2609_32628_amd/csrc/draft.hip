@@ -12,17 +12,13 @@
 
 namespace da2 {
 
-__global__ void zero_u32_kernel(uint32_t* p, int64_t stride, int count, int64_t n_rows) {
-  int64_t row = blockIdx.x;
-  for (int i = threadIdx.x; i < count; i += blockDim.x) p[row * stride + i] = 0u;
-  (void)n_rows;
-}
-
 // One workgroup per (block, head, Q or K). The block's slots are read with
 // coalesced 16-byte loads into an LDS tile (padding rows repeat the last valid
 // row); thread
 // (channel pair p, row group q) then reduces rows [q RPQ, (q + 1) RPQ) of its
-// two channels: float64 sums, float32 maxima over the valid rows and max |x|.
+// two channels: float64 sums, float32 maxima over the valid rows and max |x|
+// (written per block; the logits launch reduces it per head, which avoids
+// hundreds of workgroups contending for one atomic address).
 // The row groups are combined through LDS in order. Sums of bf16 values in
 // float64 are exact, so for bf16 inputs the order of the additions does not
 // change the mean.
@@ -95,7 +91,7 @@ __global__ __launch_bounds__(256) void draft_pool_kernel(DraftArgs args) {
   }
   if (tid == 0) {
     const float m = fmaxf(fmaxf(s_amax[0], s_amax[1]), fmaxf(s_amax[2], s_amax[3]));
-    atomic_max_pos(args.stats + (int64_t)bh * (4 + D) + which, m);
+    args.blkmax[((int64_t)which * args.B * args.H + bh) * args.R + a] = m;
   }
 }
 
@@ -157,6 +153,20 @@ __global__ __launch_bounds__(256) void draft_logits_kernel(DraftArgs args) {
 #pragma unroll
       for (int j = 0; j < NI; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[cur][i].y, b[cur][j].y, acc[i][j], 0, 0, 0);
+  }
+  // workgroup (0, 0, 2 head + branch) also reduces the per-block max |Q|
+  // (branch 0) or max |K| (branch 1) of its head into the statistics entry
+  if (blockIdx.x == 0 && blockIdx.y == 0) {
+    __shared__ float s_red[4];
+    const float* bm = args.blkmax + ((int64_t)br * args.B * args.H + bh) * R;
+    float m = 0.0f;
+    for (int i = threadIdx.x; i < R; i += 256) m = fmaxf(m, bm[i]);
+    m = wave_max(m);
+    if (lane == 0) s_red[wave] = m;
+    __syncthreads();
+    if (threadIdx.x == 0)
+      args.stats[(int64_t)bh * (4 + d) + br] =
+          __float_as_uint(fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3])));
   }
   // accumulator element e of lane l: row l/16 + 4e, column l%16
   const double sqd = sqrt((double)d);
@@ -250,8 +260,6 @@ __global__ __launch_bounds__(256) void draft_softmax_kernel(DraftArgs args) {
 
 hipError_t launch_draft(const DraftArgs& args, hipStream_t stream) {
   const int BH = args.B * args.H;
-  hipLaunchKernelGGL(zero_u32_kernel, dim3(BH), dim3(64), 0, stream, args.stats, (int64_t)(4 + args.d), 2,
-                     (int64_t)BH);
   const dim3 pool_grid(args.R, BH, 2);
   if (args.d == 128) {
     if (args.dtype == DA2_BF16)

@@ -65,7 +65,7 @@ void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
   const int64_t e = d.BH * d.Npad * d.d;
   s->ops_bytes = 3 * align_up(2 * e) + 3 * align_up(e) + 2 * align_up(4 * d.BH * d.R) + align_up(4 * d.BH * d.d) +
                  align_up(16 * d.BH) + 3 * align_up(2 * e) + 3 * align_up(mx_block_bytes(d) * d.BH * d.R);
-  s->ws_draft_bytes = 4 * align_up(8 * d.BH * d.R * d.d) + 2 * align_up(8 * d.BH * d.R * d.R);
+  s->ws_draft_bytes = 4 * align_up(8 * d.BH * d.R * d.d) + 2 * align_up(8 * d.BH * d.R * d.R) + align_up(8 * d.BH * d.R);
   int64_t thr = scope == DA2_SCOPE_ROW ? 8 * da2::kCuts * d.BH * d.R : 8 * da2::kCuts * d.BH;
   s->ws_rank_bytes = align_up(4 * d.BH * da2::kCuts * 2048) + align_up(thr) + align_up(8 * da2::kCuts * d.BH) +
                      align_up(8 * da2::kCuts * d.BH) + align_up(4 * d.BH * d.R) +
@@ -97,6 +97,7 @@ void draft_offsets(const Dims& d, int64_t* off) {
   for (int i = 0; i < 4; ++i) off[i] = i * pooled;
   off[4] = 4 * pooled;
   off[5] = 4 * pooled + logits;
+  off[6] = 4 * pooled + 2 * logits;
 }
 
 int32_t check_tensor(const da2_tensor* t, const Dims& d, bool out) {
@@ -278,7 +279,7 @@ int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const 
   sizes_of(d, DA2_SCOPE_HEAD, &sz);
   if (ws_bytes < sz.ws_draft_bytes) return DA2_ERR_WORKSPACE;
   if ((st = check_device())) return st;
-  int64_t off[6];
+  int64_t off[7];
   draft_offsets(d, off);
   char* w = static_cast<char*>(ws);
   da2::DraftArgs a{};
@@ -303,6 +304,7 @@ int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const 
   a.Kmax = reinterpret_cast<double*>(w + off[3]);
   a.S1 = reinterpret_cast<double*>(w + off[4]);
   a.S2 = reinterpret_cast<double*>(w + off[5]);
+  a.blkmax = reinterpret_cast<float*>(w + off[6]);
   return hip_status(da2::launch_draft(a, static_cast<hipStream_t>(stream)));
 }
 

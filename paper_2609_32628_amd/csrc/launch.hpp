@@ -18,6 +18,7 @@ struct DraftArgs {
   float* A;
   uint32_t* stats;
   double *Qbar, *Qmax, *Kbar, *Kmax, *S1, *S2;
+  float* blkmax;  // [2][B*H][R]: max |Q| (then |K|) of each block
 };
 
 constexpr int kCuts = 3;  // rank cut points: T16, T16+T8, T16+T8+T4

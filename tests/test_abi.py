@@ -60,7 +60,8 @@ def test_sizes_mid_layer():
     lo = api.da2_lists_offsets(_p(configs.MID))
     assert lo[1] >= 2 * 12 * 588 * 588 and lo[2] - lo[1] >= 16 * 12 * 588 and s["lists_bytes"] >= lo[3] + 32
     wo = api.da2_ws_draft_offsets(_p(configs.MID))
-    assert s["ws_draft_bytes"] >= wo[5] + 8 * 12 * 588 * 588
+    assert wo[6] >= wo[5] + 8 * 12 * 588 * 588 and len(wo) == 7
+    assert s["ws_draft_bytes"] >= wo[6] + 2 * 4 * 12 * 588
 
 
 @pytest.mark.parametrize("T,Hg,Wg", [(2, 16, 16), (2, 13, 11), (3, 7, 17), (21, 30, 52)])
