@@ -31,8 +31,10 @@ __global__ __launch_bounds__(256) void draft_pool_kernel(DraftArgs args) {
   constexpr int RQ = 256 / CP;           // row groups of the reduction
   constexpr int RPQ = kCap / RQ;         // rows per group
   __shared__ __align__(16) T tile[kCap * D];
-  __shared__ double s_sum[RQ][D];
-  __shared__ float s_max[RQ][D];
+  // the per-group partial sums and maxima reuse the tile once it is read
+  static_assert(RQ * D * (sizeof(double) + sizeof(float)) <= sizeof(T) * kCap * D, "partials fit in the tile");
+  double (*s_sum)[D] = reinterpret_cast<double (*)[D]>(tile);
+  float (*s_max)[D] = reinterpret_cast<float (*)[D]>(reinterpret_cast<char*>(tile) + RQ * D * sizeof(double));
   __shared__ float s_amax[4];
   const int a = blockIdx.x, bh = blockIdx.y, which = blockIdx.z;
   const int b = bh / args.H, h = bh % args.H, tid = threadIdx.x;
@@ -70,6 +72,7 @@ __global__ __launch_bounds__(256) void draft_pool_kernel(DraftArgs args) {
     m1 = fmaxf(m1, f.y);
     am = fmaxf(am, fmaxf(fabsf(f.x), fabsf(f.y)));
   }
+  __syncthreads();  // every thread is done with the tile
   s_sum[q][2 * p] = s0;
   s_sum[q][2 * p + 1] = s1;
   s_max[q][2 * p] = m0;
