@@ -33,7 +33,9 @@
  *   tokens in row-major order, then padding.
  * - Every device buffer is allocated and owned by the caller; sizes come from
  *   da2_sizes(). The library never allocates or frees device memory, never
- *   synchronizes the host and keeps no mutable global state. Buffers that a
+ *   synchronizes the host and keeps no mutable global state (the one
+ *   exception is the fixed per-device scratch array that
+ *   da2_rank_assign_noalloc uses instead of a workspace). Buffers that a
  *   call writes must not be read or written by other work on other streams
  *   until the call has completed on its stream.
  * - "device" pointers must be device-accessible (hipMalloc / torch cuda
@@ -165,6 +167,25 @@ int32_t da2_ws_draft_offsets(const da2_problem* p, int64_t* offsets7);
 int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int32_t num8,
                         int32_t num4, int32_t den, int32_t scope, uint8_t* cls, void* lists,
                         void* ws, int64_t ws_bytes, void* stream);
+
+/* Allocation-free variant of da2_rank_assign, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, results and errors as
+ * da2_rank_assign, except that no workspace is passed: the ranking's
+ * workspace is a fixed device array of DA2_RANK_NOALLOC_MAX_BYTES inside the
+ * library (one copy per device, held until the process ends; its address is
+ * looked up once per device on the first call there). The call allocates
+ * nothing and clears what must start at zero with kernels.
+ *   Errors: DA2_ERR_WORKSPACE when the problem's ws_rank_bytes (da2_sizes)
+ *   exceeds DA2_RANK_NOALLOC_MAX_BYTES; DA2_ERR_HIP when the array's device
+ *   address cannot be looked up.
+ * Calls on one device share the array: two such calls that overlap in time on
+ * the same device (different streams or threads without ordering) race and
+ * give undefined results. Calls on different devices do not interact. */
+#define DA2_RANK_NOALLOC_MAX_BYTES (8ll << 20)
+int32_t da2_rank_assign_noalloc(const float* A, const da2_problem* p, int32_t num16, int32_t num8,
+                                int32_t num4, int32_t den, int32_t scope, uint8_t* cls, void* lists,
+                                void* stream);
 
 /* Offsets (bytes) inside lists:
  *   [0] keys   uint16 [B*H*R][R]: row (b,h,a) holds its 4-bit key blocks

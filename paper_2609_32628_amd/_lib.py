@@ -14,10 +14,11 @@ DA2_BF16, DA2_FP32 = 0, 1
 DA2_SCOPE_HEAD, DA2_SCOPE_ROW = 0, 1
 DA2_PART_TILES8, DA2_PART_RAGGED = 0, 1
 DA2_FMT4_NVFP4, DA2_FMT4_MXFP4 = 0, 1
+DA2_RANK_NOALLOC_MAX_BYTES = 8 << 20   # include/da2.h
 
 # Every symbol include/da2.h declares.
 EXPORTS = ("da2_status_string", "da2_sizes", "da2_layout_build", "da2_draft_map", "da2_ws_draft_offsets",
-           "da2_rank_assign", "da2_lists_offsets", "da2_prep_operands", "da2_ops_offsets", "da2_mixed_attn")
+           "da2_rank_assign", "da2_rank_assign_noalloc", "da2_lists_offsets", "da2_prep_operands", "da2_ops_offsets", "da2_mixed_attn")
 
 
 class Problem(ctypes.Structure):
@@ -66,6 +67,7 @@ def lib():
             "da2_draft_map": (i32, [vp, vp, T, vp, P, dbl, vp, vp, vp, i64, vp]),
             "da2_ws_draft_offsets": (i32, [P, pi64]),
             "da2_rank_assign": (i32, [vp, P, i32, i32, i32, i32, i32, vp, vp, vp, i64, vp]),
+            "da2_rank_assign_noalloc": (i32, [vp, P, i32, i32, i32, i32, i32, vp, vp, vp]),
             "da2_lists_offsets": (i32, [P, pi64]),
             "da2_prep_operands": (i32, [vp, vp, vp, T, vp, P, i32, i32, vp, vp, vp, i64, vp]),
             "da2_ops_offsets": (i32, [P, pi64]),

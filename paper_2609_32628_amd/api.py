@@ -87,6 +87,11 @@ def da2_rank_assign(A, p, num16, num8, num4, den, scope, cls, lists, ws, stream=
         ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def da2_rank_assign_noalloc(A, p, num16, num8, num4, den, scope, cls, lists, stream=None):
+    check("da2_rank_assign_noalloc", lib().da2_rank_assign_noalloc(
+        _ptr(A), ctypes.byref(p), num16, num8, num4, den, SCOPES[scope], _ptr(cls), _ptr(lists), _stream(stream)))
+
+
 def da2_prep_operands(Q, K, V, layout, p, with16, fmt4, stats, ops, ws, stream=None):
     if not (Q.shape == K.shape == V.shape and Q.stride() == K.stride() == V.stride() and Q.dtype == K.dtype == V.dtype):
         raise ValueError("Q, K and V must share shape, strides and dtype")

@@ -308,22 +308,28 @@ int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const 
   return hip_status(da2::launch_draft(a, static_cast<hipStream_t>(stream)));
 }
 
-int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int32_t num8, int32_t num4,
-                        int32_t den, int32_t scope, uint8_t* cls, void* lists, void* ws, int64_t ws_bytes,
-                        void* stream) {
-  Dims d;
-  int32_t st = derive(p, &d);
+}  // extern "C"
+
+namespace {
+
+// Validation shared by both ranking entry points (everything but the workspace).
+int32_t rank_check(const float* A, const da2_problem* p, int32_t num16, int32_t num8, int32_t num4, int32_t den,
+                   int32_t scope, const uint8_t* cls, const void* lists, Dims* d) {
+  int32_t st = derive(p, d);
   if (st) return st;
-  if (!A || !cls || !lists || !ws) return DA2_ERR_INVALID_ARG;
+  if (!A || !cls || !lists) return DA2_ERR_INVALID_ARG;
   if (den <= 0 || num16 < 0 || num8 < 0 || num4 < 0 || (int64_t)num16 + num8 + num4 > den)
     return DA2_ERR_INVALID_ARG;
   if (scope != DA2_SCOPE_HEAD && scope != DA2_SCOPE_ROW) return DA2_ERR_INVALID_ARG;
-  if (scope == DA2_SCOPE_HEAD && d.R * d.R >= (1ll << 22)) return DA2_ERR_INVALID_ARG;
-  if (scope == DA2_SCOPE_ROW && d.R > 8192) return DA2_ERR_UNSUPPORTED;
-  da2_sizes_t sz;
-  sizes_of(d, scope, &sz);
-  if (ws_bytes < sz.ws_rank_bytes) return DA2_ERR_WORKSPACE;
-  if ((st = check_device())) return st;
+  if (scope == DA2_SCOPE_HEAD && d->R * d->R >= (1ll << 22)) return DA2_ERR_INVALID_ARG;
+  if (scope == DA2_SCOPE_ROW && d->R > 8192) return DA2_ERR_UNSUPPORTED;
+  return DA2_OK;
+}
+
+// The ranking launch on a validated problem with workspace ws (at least
+// ws_rank_bytes, 256-byte aligned).
+int32_t rank_launch(const float* A, const Dims& d, int32_t num16, int32_t num8, int32_t num4, int32_t den,
+                    int32_t scope, uint8_t* cls, void* lists, void* ws, void* stream) {
   const int64_t M = scope == DA2_SCOPE_HEAD ? d.R * d.R : d.R;
   // cumulative quotas, rounded half up: ranks [0, cut0) -> 16, [cut0, cut1) -> 8, [cut1, cut2) -> 4
   auto half_up = [&](int64_t num) { return (2 * num * M + den) / (2 * (int64_t)den); };
@@ -361,6 +367,39 @@ int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int
   o += align_up(8 * d.BH * da2::kCuts * da2::kRankCand);
   a.ccount = reinterpret_cast<uint32_t*>(w + o);
   return hip_status(da2::launch_rank(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int32_t num8, int32_t num4,
+                        int32_t den, int32_t scope, uint8_t* cls, void* lists, void* ws, int64_t ws_bytes,
+                        void* stream) {
+  Dims d;
+  int32_t st = rank_check(A, p, num16, num8, num4, den, scope, cls, lists, &d);
+  if (st) return st;
+  if (!ws) return DA2_ERR_INVALID_ARG;
+  da2_sizes_t sz;
+  sizes_of(d, scope, &sz);
+  if (ws_bytes < sz.ws_rank_bytes) return DA2_ERR_WORKSPACE;
+  if ((st = check_device())) return st;
+  return rank_launch(A, d, num16, num8, num4, den, scope, cls, lists, ws, stream);
+}
+
+int32_t da2_rank_assign_noalloc(const float* A, const da2_problem* p, int32_t num16, int32_t num8, int32_t num4,
+                                int32_t den, int32_t scope, uint8_t* cls, void* lists, void* stream) {
+  Dims d;
+  int32_t st = rank_check(A, p, num16, num8, num4, den, scope, cls, lists, &d);
+  if (st) return st;
+  da2_sizes_t sz;
+  sizes_of(d, scope, &sz);
+  static_assert(da2::kRankScratchBytes == DA2_RANK_NOALLOC_MAX_BYTES, "header limit and scratch size agree");
+  if (sz.ws_rank_bytes > da2::kRankScratchBytes) return DA2_ERR_WORKSPACE;
+  if ((st = check_device())) return st;
+  void* ws = nullptr;
+  if (da2::rank_scratch_address(&ws) != hipSuccess) return DA2_ERR_HIP;
+  return rank_launch(A, d, num16, num8, num4, den, scope, cls, lists, ws, stream);
 }
 
 int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv, const int32_t* layout,

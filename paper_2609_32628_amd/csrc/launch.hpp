@@ -83,6 +83,12 @@ struct AttnArgs {
   int odtype;
 };
 
+// Size of the fixed device scratch that da2_rank_assign_noalloc uses instead
+// of a caller workspace (8 MiB per device).
+constexpr int64_t kRankScratchBytes = 8ll << 20;
+// Device address of the current device's scratch array (looked up once per device).
+hipError_t rank_scratch_address(void** out);
+
 hipError_t launch_draft(const DraftArgs& args, hipStream_t stream);
 hipError_t launch_rank(const RankArgs& args, hipStream_t stream);
 hipError_t launch_prep(const PrepArgs& args, hipStream_t stream);

@@ -16,6 +16,8 @@
 // kRankCand of them, its scan sorts them and reads the threshold key directly,
 // and the last two passes skip that cut. Row scope sorts each row's R keys in
 // LDS (bitonic).
+#include <mutex>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -420,6 +422,37 @@ __global__ __launch_bounds__(1024) void rank_order_kernel(RankArgs args) {
     args.order[pos] = (int32_t)i;
   }
   if (threadIdx.x == 0) args.meta[0] = (int32_t)n;
+}
+
+// Fixed device scratch for callers that cannot allocate (da2_rank_assign_noalloc):
+// every workspace array of the ranking lives here instead of in a caller
+// buffer. Each device holds its own copy for the life of the process; calls
+// on one device share it, so such calls must not overlap on that device. The
+// kernels clear what must start at zero (rank_init_kernel), so no state from
+// an earlier call is read.
+static __device__ __align__(256) uint8_t scratch[kRankScratchBytes];
+
+// Device address of this device's copy of the scratch array, looked up once
+// per device with that device current and then reused. In host code the
+// array's name is only a stand-in for the symbol, never a device address.
+hipError_t rank_scratch_address(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_rank(const RankArgs& args, hipStream_t stream) {
