@@ -143,7 +143,11 @@ def run_sweep(args):
         dev.append(X)
     del heads
     p = api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg, w.partition)
-    buf = api.alloc(p, "head")
+    buf = api.alloc(p, "head", with16=True)
+    # the operand buffer of each 4-bit encoding (sized for the 16-bit path too)
+    ops_of = {"nvfp4": buf.ops,
+              "mxfp4": torch.empty(api.da2_sizes(p, "head", "mxfp4", True)["ops_bytes"], dtype=torch.uint8,
+                                   device="cuda")}
     O = torch.empty(dev[0].shape, dtype=torch.bfloat16, device="cuda")
     stream = torch.cuda.current_stream()
     idx_h = torch.tensor(ref_heads, device="cuda")
@@ -153,11 +157,11 @@ def run_sweep(args):
         def step(ev=None):
             api.da2_draft_map(dev[0], dev[1], buf.layout, p, lam, buf.A, buf.stats, buf.ws_draft)
             api.da2_rank_assign(buf.A, p, n16, n8, n4, SWEEP_DEN, "head", buf.cls, buf.lists, buf.ws_rank)
-            api.da2_prep_operands(dev[0], dev[1], dev[2], buf.layout, p, int(n16 > 0), fmt4, buf.stats, buf.ops,
-                                  None)
+            api.da2_prep_operands(dev[0], dev[1], dev[2], buf.layout, p, int(n16 > 0), fmt4, buf.stats,
+                                  ops_of[fmt4], None)
             if ev is not None:
                 ev[0].record(stream)
-            api.da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, fmt4=fmt4)
+            api.da2_mixed_attn(ops_of[fmt4], buf.lists, buf.layout, p, O, fmt4=fmt4)
             if ev is not None:
                 ev[1].record(stream)
 
@@ -268,7 +272,7 @@ def main():
     Q, K, V = gen.generate(w)
     dev = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (Q, K, V)]
     p = api.problem(w.B, w.H, w.d, w.T, w.Hg, w.Wg, w.partition)
-    buf = api.alloc(p, w.scope)
+    buf = api.alloc(p, w.scope, fmt4=args.fmt4, with16=w.num16 > 0)
     O = torch.empty(dev[0].shape, dtype=torch.bfloat16, device="cuda")
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -360,11 +364,10 @@ def main():
     sizes = buf.sizes
     e_in = w.B * w.H * w.N * w.d * 2
     draft_bytes = 2 * e_in + sizes["A_bytes"]
-    # sections prep_operands writes: 8-bit operands and scales, the 4-bit
-    # encoding in use, and the 16-bit operands only when that path is on
-    off = api.da2_ops_offsets(p) + [sizes["ops_bytes"]]
-    written = [3, 4, 5, 6, 7, 8, 9] + ([13, 14, 15] if mx else [0, 1, 2]) + ([10, 11, 12] if w.num16 > 0 else [])
-    prep_bytes = 3 * e_in + sum(off[i + 1] - off[i] for i in written)
+    # the ops buffer holds exactly the sections prep_operands writes: 8-bit
+    # operands and scales, the 4-bit encoding in use, and the 16-bit operands
+    # only when that path is on
+    prep_bytes = 3 * e_in + sizes["ops_bytes"]
     t_draft, t_prep = stage_ms["draft_map"] * 1e-3, stage_ms["prep_operands"] * 1e-3
     hbm = {"draft_map": {"bytes": draft_bytes, "GB/s": draft_bytes / t_draft / 1e9,
                          "frac": draft_bytes / t_draft / PEAK_HBM},

@@ -45,7 +45,7 @@
  *   Launch failures return DA2_ERR_HIP. Nothing is written when validation
  *   fails.
  * - Only gfx950 devices are supported (DA2_ERR_UNSUPPORTED otherwise). Head
- *   dimension d must be 64 or 128.
+ *   dimension d must be 64 or 128 (DA2_ERR_UNSUPPORTED otherwise).
  */
 #ifndef DA2_H
 #define DA2_H
@@ -109,15 +109,32 @@ typedef struct {
   int64_t ws_draft_bytes, ws_rank_bytes, ws_prep_bytes;
 } da2_sizes_t;
 
+/* Version of the documented layouts of the ops and lists buffers
+ * (da2_ops_offsets, da2_lists_offsets). Version 2: packed NVFP4 sections,
+ * sections sized and ordered by (fmt4, with16), encoding tag in g word 3. */
+#define DA2_OPS_LAYOUT_VERSION 2
+
+/* Error flags that da2_mixed_attn ORs into word 1 of the lists meta area
+ * (da2_lists_offsets [3]) when the operands do not match the call; the rows
+ * concerned are written as zeros. */
+#define DA2_ATTN_ERR_LAYOUT 1u /* ops not written by this layout version (or never written) */
+#define DA2_ATTN_ERR_FMT4 2u   /* ops prepared with another fmt4 */
+#define DA2_ATTN_ERR_NO16 4u   /* a row has 16-bit blocks but ops were prepared with with16 = 0 */
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* da2_status_string(int32_t status);
 
-/* Host only. Fills *out for problem p; ranking scope affects ws_rank_bytes.
- * Errors: INVALID_ARG for non-positive dims, d not in {64,128}, an unknown
- * partition, or sizes that
- * overflow the index types or launch grids (R > 65535 blocks, B*H > 32767,
- * B*H*R > 2^31-1). */
-int32_t da2_sizes(const da2_problem* p, int32_t scope, da2_sizes_t* out);
+/* Host only. Fills *out for problem p. The ranking scope sets ws_rank_bytes;
+ * fmt4 (da2_fmt4) and with16 (0 or 1) set ops_bytes: the ops buffer holds only
+ * the sections a run with that 4-bit encoding and 16-bit option writes.
+ * Errors: INVALID_ARG for non-positive dims, an unknown partition, scope,
+ * fmt4 or with16, or sizes that overflow the index types or launch grids
+ * (R > 65535 blocks, B*H > 32767, B*H*R > 2^31-1); UNSUPPORTED for a head
+ * dimension d other than 64 or 128 (every entry point that takes p). */
+int32_t da2_sizes(const da2_problem* p, int32_t scope, int32_t fmt4, int32_t with16, da2_sizes_t* out);
+
+/* DA2_OPS_LAYOUT_VERSION of the library (host only). */
+int32_t da2_ops_layout_version(void);
 
 /* Host only: region layout (fused-preparation section: each region packed
  * into one contiguous block, valid counts n_a, inverse index map).
@@ -197,7 +214,9 @@ int32_t da2_rank_assign_noalloc(const float* A, const da2_problem* p, int32_t nu
  *              by head and by row parity, most expensive first in each group;
  *              attention workgroup w takes order[(w mod 8)*ceil(n/8) + w div 8]
  *              (any permutation of the rows is a valid order)
- *   [3] meta   int32 [8]: [0] = number of rows in order                       */
+ *   [3] meta   int32 [8]: [0] = number of rows in order; [1] = error flags
+ *              (DA2_ATTN_ERR_*) of da2_mixed_attn calls on these lists,
+ *              cleared by da2_rank_assign                                  */
 int32_t da2_lists_offsets(const da2_problem* p, int64_t* offsets4);
 
 /* Operand preparation (format appendix; NVFP4 quantization equation):
@@ -208,9 +227,10 @@ int32_t da2_lists_offsets(const da2_problem* p, int64_t* offsets4);
  *   NVFP4 Q, K (16-channel groups) and V (16 key slots per channel):
  *     g = f32(amax_head / 2688) (1 if zero), sigma = E4M3_rne(f32(amax_G /
  *     f32(6 g))), e = E2M1_rne(f32(x * f32(1 / f32(g sigma)))); sigma == 0 ->
- *     zeros. Stored as the exact fp16 value sigma*e (gfx950 has no MFMA that
- *     applies E4M3 scales per 16 elements; sigma*e has at most 6 significant
- *     bits, so fp16 holds it exactly and fp16 MFMA reproduces the products).
+ *     zeros. Stored as 4-bit E2M1 codes with one E4M3 scale byte per group
+ *     (4.5 bits per value); the attention decodes sigma*e to fp16 (exact: at
+ *     most 6 significant bits), since gfx950 has no MFMA that applies E4M3
+ *     scales per 16 elements.
  *   FP16 Q, K, V (16-bit path, INT8 and FP16 paragraph): the values rounded
  *     to nearest-even half precision; written only when with16 = 1.
  *   MXFP4 Q, K (32-channel blocks) and V (32 key slots per channel), written
@@ -224,29 +244,51 @@ int32_t da2_lists_offsets(const da2_problem* p, int64_t* offsets4);
  *   with16   0 or 1: also write the 16-bit sections [10..12] of ops. A
  *            da2_mixed_attn call whose lists hold 16-bit blocks needs them.
  *   fmt4     da2_fmt4: NVFP4 writes sections [0..2], MXFP4 sections
- *            [13..15]; the other 4-bit sections are left untouched, and
- *            da2_mixed_attn must be called with the same fmt4.
- *   ops      device out, ops_bytes (see da2_ops_offsets)
- * Errors: INVALID_ARG for with16 or fmt4 out of range, misaligned inputs.   */
+ *            [13..15]; da2_mixed_attn must be called with the same fmt4.
+ *            The call writes the tag (0xDA200000 | DA2_OPS_LAYOUT_VERSION << 8
+ *            | with16 << 4 | fmt4) into word 3 of each head's g entry, which
+ *            da2_mixed_attn checks.
+ *   ops      device out of ops_bytes bytes, at least ops_bytes of
+ *            da2_sizes(p, scope, fmt4, with16) (section offsets:
+ *            da2_ops_offsets(p, fmt4, with16))
+ * Errors: INVALID_ARG for with16 or fmt4 out of range, misaligned inputs, or
+ * ops_bytes below the size the (fmt4, with16) sections need.                */
 int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv,
                           const int32_t* layout, const da2_problem* p, int32_t with16, int32_t fmt4,
-                          void* stats, void* ops, void* ws, int64_t ws_bytes, void* stream);
+                          void* stats, void* ops, int64_t ops_bytes, void* ws, int64_t ws_bytes,
+                          void* stream);
 
-/* Offsets (bytes) inside ops, per section; each section is [B*H][R][...]
- * with one 64-slot block per R, in the fragment order of the gfx950 MFMA
- * tiles the attention kernel consumes (lane = 0..63, g = lane/32):
- *   [0] Q4  fp16 [qt:2][s:d/16][lane][8]  = sigma*e of Q[slot 32qt+lane%32][16s+8g+e]
- *   [1] K4  fp16 [j:2][s:d/16][lane][8]   = sigma*e of K[kappa(j,lane%32)][16s+8g+e]
- *   [2] V4  fp16 [t:d/32][s:4][lane][8]   = sigma*e of V[32(s/2)+16g+8(s%2)+e][32t+lane%32]
+/* Offsets (bytes) inside ops of the 16 sections, for a run with (fmt4,
+ * with16); -1 for a section such a run neither writes nor reads. The buffer
+ * holds, in this order: the 8-bit sections and the scales [3..9], the 4-bit
+ * encoding in use ([0..2] for NVFP4, [13..15] for MXFP4), then the 16-bit
+ * sections [10..12] when with16 = 1 (so no other offset depends on with16).
+ * Each section is [B*H][R][...] with one 64-slot block per R; lane = 0..63,
+ * g = lane/32, r = lane%32, NS = d/16, NT = d/32; "fragment" means the
+ * 16-byte-per-lane operand of a gfx950 32x32 MFMA:
+ *   [0] Q4, [1] K4, [2] V4  packed NVFP4, 36 d bytes per block: 32 d bytes of
+ *        E2M1 codes (code e of a dword in nibble e, sign bit 3), then 4 d bytes
+ *        of E4M3 scale codes. Ordered by the attention thread (wave w = 0,1,
+ *        lane) that decodes them into the fp16 fragments
+ *          Q: [qt:2][s:NS][lane][8] = sigma*e of Q[slot 32qt + r][16s + 8g + e]
+ *          K: [j:2][s:NS][lane][8]  = sigma*e of K[kappa(j, r)][16s + 8g + e]
+ *          V: [t:NT][s:4][lane][8]  = sigma*e of V[32(s/2)+16g+8(s%2)+e][32t + r]:
+ *        codes: dword (w*64 + lane)*NS + f holds the 8 codes of fragment f of
+ *          that thread: Q, K fragment (w, s = f); V fragment (t = w*NT/2 + f/4,
+ *          s = f%4);
+ *        scales: Q, K byte 32d + (w*32 + r)*NS + s = sigma of row (w, r),
+ *          channel group s; V byte 32d + (w*64 + lane)*NT/2*2 + 2*t2 + h =
+ *          sigma of channel 32t + r (t = w*NT/2 + t2), key group 2h + g.
  *   [3] Q8  int8 [qt:2][s:d/32][lane][16] = code of Q[slot 32qt+lane%32][32s+16g+e]
  *   [4] K8  int8 [j:2][s:d/32][lane][16]  = code of K[kappa(j,lane%32)][32s+16g+e]
  *   [5] V8  e4m3 [t:d/32][h:2][lane][16]  = code of V[32h+16g+e][32t+lane%32]
  *   [6] dQ  float32 [B*H][R]   INT8 scale of each query block
  *   [7] dK  float32 [B*H][R]   INT8 scale of each key block
  *   [8] dV  float32 [B*H][d]   E4M3 per-channel scale of V
- *   [9] g   float32 [B*H][4]   (g_Q, g_K, g_V, 0) NVFP4 tensor scales
- *   [10] Q16, [11] K16, [12] V16  fp16, the layouts of Q4, K4, V4 holding the
- *            half-precision values of the 16-bit path
+ *   [9] g   float32 [B*H][4]   (g_Q, g_K, g_V, tag) NVFP4 tensor scales and the
+ *            encoding tag (uint32 bits, see da2_prep_operands)
+ *   [10] Q16, [11] K16, [12] V16  fp16, the half-precision values of the
+ *            16-bit path in the fp16 fragment orders of Q, K, V above
  *   [13] Q4mx, [14] K4mx, [15] V4mx  MXFP4 operands, (d/32 + 1) fragments of
  *            1 KB per block: d/32 data fragments, then one scale fragment.
  *            Code i (0..31) of a lane sits in byte i/2 of the lane's 16 bytes,
@@ -261,8 +303,8 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
  * that puts each 16-slot group of a query row into one lane, see the operand
  * permutation equation) and kappa_mx(j, r) = 32((r/4)%2) + 16j + 4(r/8) + r%4
  * (the one that puts each 32-slot MXFP4 block of a query row into one lane
- * half). */
-int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets16);
+ * half). Errors: INVALID_ARG for fmt4 or with16 out of range. */
+int32_t da2_ops_offsets(const da2_problem* p, int32_t fmt4, int32_t with16, int64_t* offsets16);
 
 /* Phased mixed-precision attention (phased-execution appendix;
  * precision-state-conversion equation). For each query block a (one
@@ -271,7 +313,8 @@ int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets16);
  * denominator l and numerator U:
  *   s = Qhat Khat^T / sqrt d; m_j = max(m_{j-1}, rowmax_j s); Pt = exp(s - m_j)
  *   4-bit: l += sum Pt; sigma_P = E4M3(448 max_16 Pt); U += (sigma_P/2688)
- *          E2M1(2688 Pt/sigma_P) Vhat4 (fp16 MFMA on sigma*e operands)
+ *          E2M1(2688 Pt/sigma_P) Vhat4 (fp16 MFMA on sigma*e operands decoded
+ *          from the packed NVFP4 sections)
  *   Enter: U_c /= eta delta_c, l /= eta   (eta = 2^-8.807)
  *   8-bit: int8 MFMA logits; P = 2^((s - m) log2 e + 8.807); l += sum P;
  *          U += E4M3(P) V8 (fp8 MFMA)
@@ -284,12 +327,18 @@ int32_t da2_ops_offsets(const da2_problem* p, int64_t* offsets16);
  *          k = floor(log2 max Pt) - 2 (clamped at -127); U += 2^k
  *          E2M1(Pt 2^-k) Vhat4 (scaled fp4 MFMA), already in the common units
  *          (no factor g_V/2688 to restore).
- *   ops, lists, layout  device, from the calls above
+ *   ops, lists, layout  device, from the calls above; ops_bytes is the size
+ *            of the ops buffer (at least da2_sizes(p, ., fmt4, 0).ops_bytes)
  *   fmt4     da2_fmt4 used by da2_prep_operands for these ops
  *   out      descriptor of O (dtype fp32 or bf16)
  *   O        device out [B,H,N,d]; every token row is written.
- * Errors: INVALID_ARG for fmt4 out of range or a bad descriptor.           */
-int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout,
+ * The kernel checks each head's tag in g word 3 against this version and
+ * fmt4, and a row with 16-bit blocks against the tag's with16 bit; a row
+ * that fails is written as zeros and the failure ORed into lists meta word 1
+ * (DA2_ATTN_ERR_*), so a mismatch is detectable after the stream completes.
+ * Errors: INVALID_ARG for fmt4 out of range, a bad descriptor or an ops
+ * buffer smaller than the sections of a run without the 16-bit path.       */
+int32_t da2_mixed_attn(const void* ops, int64_t ops_bytes, const void* lists, const int32_t* layout,
                        const da2_problem* p, int32_t fmt4, const da2_tensor* out, void* O,
                        void* stream);
 

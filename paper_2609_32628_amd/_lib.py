@@ -15,9 +15,12 @@ DA2_SCOPE_HEAD, DA2_SCOPE_ROW = 0, 1
 DA2_PART_TILES8, DA2_PART_RAGGED = 0, 1
 DA2_FMT4_NVFP4, DA2_FMT4_MXFP4 = 0, 1
 DA2_RANK_NOALLOC_MAX_BYTES = 8 << 20   # include/da2.h
+DA2_OPS_LAYOUT_VERSION = 2
+DA2_ATTN_ERR_LAYOUT, DA2_ATTN_ERR_FMT4, DA2_ATTN_ERR_NO16 = 1, 2, 4
+TAG_MARKER = 0xDA200000   # encoding tag in word 3 of each head's g entry
 
 # Every symbol include/da2.h declares.
-EXPORTS = ("da2_status_string", "da2_sizes", "da2_layout_build", "da2_draft_map", "da2_ws_draft_offsets",
+EXPORTS = ("da2_status_string", "da2_sizes", "da2_ops_layout_version", "da2_layout_build", "da2_draft_map", "da2_ws_draft_offsets",
            "da2_rank_assign", "da2_rank_assign_noalloc", "da2_lists_offsets", "da2_prep_operands", "da2_ops_offsets", "da2_mixed_attn")
 
 
@@ -62,16 +65,17 @@ def lib():
         pi64, pi32 = ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int32)
         sig = {
             "da2_status_string": (ctypes.c_char_p, [i32]),
-            "da2_sizes": (i32, [P, i32, S]),
+            "da2_sizes": (i32, [P, i32, i32, i32, S]),
+            "da2_ops_layout_version": (i32, []),
             "da2_layout_build": (i32, [P, pi32, i64]),
             "da2_draft_map": (i32, [vp, vp, T, vp, P, dbl, vp, vp, vp, i64, vp]),
             "da2_ws_draft_offsets": (i32, [P, pi64]),
             "da2_rank_assign": (i32, [vp, P, i32, i32, i32, i32, i32, vp, vp, vp, i64, vp]),
             "da2_rank_assign_noalloc": (i32, [vp, P, i32, i32, i32, i32, i32, vp, vp, vp]),
             "da2_lists_offsets": (i32, [P, pi64]),
-            "da2_prep_operands": (i32, [vp, vp, vp, T, vp, P, i32, i32, vp, vp, vp, i64, vp]),
-            "da2_ops_offsets": (i32, [P, pi64]),
-            "da2_mixed_attn": (i32, [vp, vp, vp, P, i32, T, vp, vp]),
+            "da2_prep_operands": (i32, [vp, vp, vp, T, vp, P, i32, i32, vp, vp, i64, vp, i64, vp]),
+            "da2_ops_offsets": (i32, [P, i32, i32, pi64]),
+            "da2_mixed_attn": (i32, [vp, i64, vp, vp, P, i32, T, vp, vp]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)

@@ -42,10 +42,14 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def da2_sizes(p, scope="head"):
+def da2_sizes(p, scope="head", fmt4="nvfp4", with16=False):
     s = _lib.Sizes()
-    check("da2_sizes", lib().da2_sizes(ctypes.byref(p), SCOPES[scope], ctypes.byref(s)))
+    check("da2_sizes", lib().da2_sizes(ctypes.byref(p), SCOPES[scope], FMT4[fmt4], int(with16), ctypes.byref(s)))
     return {f: getattr(s, f) for f, _ in _lib.Sizes._fields_}
+
+
+def da2_ops_layout_version():
+    return lib().da2_ops_layout_version()
 
 
 def da2_layout_build(p):
@@ -57,9 +61,9 @@ def da2_layout_build(p):
     return out
 
 
-def _offsets(fn, p, n):
+def _offsets(fn, p, n, *extra):
     arr = (ctypes.c_int64 * n)()
-    check(fn, getattr(lib(), fn)(ctypes.byref(p), arr))
+    check(fn, getattr(lib(), fn)(ctypes.byref(p), *extra, arr))
     return list(arr)
 
 
@@ -71,8 +75,10 @@ def da2_lists_offsets(p):
     return _offsets("da2_lists_offsets", p, 4)
 
 
-def da2_ops_offsets(p):
-    return _offsets("da2_ops_offsets", p, 16)
+def da2_ops_offsets(p, fmt4="nvfp4", with16=False):
+    """Byte offsets of the 16 ops sections for a run with (fmt4, with16); -1
+    for a section such a run does not use."""
+    return _offsets("da2_ops_offsets", p, 16, FMT4[fmt4], int(with16))
 
 
 def da2_draft_map(Q, K, layout, p, lam, A, stats, ws, stream=None):
@@ -98,20 +104,25 @@ def da2_prep_operands(Q, K, V, layout, p, with16, fmt4, stats, ops, ws, stream=N
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     check("da2_prep_operands", lib().da2_prep_operands(
         _ptr(Q), _ptr(K), _ptr(V), ctypes.byref(_tensor_desc(Q)), _ptr(layout), ctypes.byref(p), int(with16),
-        FMT4[fmt4], _ptr(stats), _ptr(ops), None if ws is None else _ptr(ws), ws_bytes, _stream(stream)))
+        FMT4[fmt4], _ptr(stats), _ptr(ops), ops.numel() * ops.element_size(), None if ws is None else _ptr(ws),
+        ws_bytes, _stream(stream)))
 
 
 def da2_mixed_attn(ops, lists, layout, p, O, stream=None, fmt4="nvfp4"):
     check("da2_mixed_attn", lib().da2_mixed_attn(
-        _ptr(ops), _ptr(lists), _ptr(layout), ctypes.byref(p), FMT4[fmt4], ctypes.byref(_tensor_desc(O)), _ptr(O),
-        _stream(stream)))
+        _ptr(ops), ops.numel() * ops.element_size(), _ptr(lists), _ptr(layout), ctypes.byref(p), FMT4[fmt4],
+        ctypes.byref(_tensor_desc(O)), _ptr(O), _stream(stream)))
 
 
 @dataclass
 class Buffers:
-    """Device buffers of one problem, sized by da2_sizes (allocation only)."""
+    """Device buffers of one problem, sized by da2_sizes (allocation only).
+    ``fmt4`` and ``with16`` are the 4-bit encoding and 16-bit option the ops
+    buffer is sized for."""
     p: Problem
     scope: str
+    fmt4: str
+    with16: bool
     sizes: dict
     layout: torch.Tensor
     A: torch.Tensor
@@ -123,8 +134,8 @@ class Buffers:
     ws_rank: torch.Tensor
 
 
-def alloc(p, scope="head", device="cuda"):
-    s = da2_sizes(p, scope)
+def alloc(p, scope="head", device="cuda", fmt4="nvfp4", with16=False):
+    s = da2_sizes(p, scope, fmt4, with16)
     R = s["R"]
     B, H = p.B, p.H
 
@@ -132,18 +143,23 @@ def alloc(p, scope="head", device="cuda"):
         return torch.empty(max(int(n), 1), dtype=torch.uint8, device=device)
 
     layout = torch.from_numpy(da2_layout_build(p)).to(device)
-    return Buffers(p, scope, s, layout,
+    return Buffers(p, scope, fmt4, bool(with16), s, layout,
                    A=torch.empty((B, H, R, R), dtype=torch.float32, device=device),
                    cls=torch.empty((B, H, R, R), dtype=torch.uint8, device=device),
                    stats=raw(s["stats_bytes"]), lists=raw(s["lists_bytes"]), ops=raw(s["ops_bytes"]),
                    ws_draft=raw(s["ws_draft_bytes"]), ws_rank=raw(s["ws_rank_bytes"]))
 
 
-def attention(Q, K, V, buf, lam, budgets, O, stream=None, num16=0, fmt4="nvfp4"):
+def attention(Q, K, V, buf, lam, budgets, O, stream=None, num16=0, fmt4=None):
     """The four calls in order: draft map, ranking, operand preparation,
     attention. budgets = (num8, num4, den); num16/den go to the 16-bit path;
-    fmt4 ("nvfp4" or "mxfp4") is the encoding of the 4-bit path."""
+    fmt4 ("nvfp4" or "mxfp4", default: the buffers' encoding) is the encoding
+    of the 4-bit path."""
     p = buf.p
+    fmt4 = buf.fmt4 if fmt4 is None else fmt4
+    if fmt4 != buf.fmt4 or (num16 > 0 and not buf.with16):
+        raise ValueError(f"buffers sized for fmt4={buf.fmt4}, with16={buf.with16}; asked for fmt4={fmt4}, "
+                         f"num16={num16}")
     da2_draft_map(Q, K, buf.layout, p, lam, buf.A, buf.stats, buf.ws_draft, stream)
     da2_rank_assign(buf.A, p, num16, *budgets, buf.scope, buf.cls, buf.lists, buf.ws_rank, stream)
     da2_prep_operands(Q, K, V, buf.layout, p, int(num16 > 0), fmt4, buf.stats, buf.ops, None, stream)

@@ -109,7 +109,8 @@ constexpr float kLog2_2688 = 11.392317422778760f;  // log2(6 * 448)
 // computed in stages so that they can be interleaved with matrix work:
 //   setup: sigma_P = E4M3(448 max Pt) from the group's maximum logit;
 //   exps:  y = Pt * 2688 / sigma_P from one exp2 each (the factor is folded
-//          into the exponent) and their fp32 sum;
+//          into the exponent), their fp32 sum, and E2M1(y) as 4-bit codes,
+//          converted in pairs as they are computed;
 //   pack:  w = sigma_P * E2M1(y) as fp16 pairs for the P^T operand (exact:
 //          at most 6 significant bits).
 // A zero sigma_P uses factor 1, and those y (all below 2^-18) round to E2M1
@@ -117,7 +118,7 @@ constexpr float kLog2_2688 = 11.392317422778760f;  // log2(6 * 448)
 struct Fp4Group {
   float off, scale, sum;
   f16x2 s2;
-  float y[16];
+  uint32_t code[2];  // E2M1 codes of slots [0,8) and [8,16), two per byte
 };
 // E4M3 value of a in [0, 448]: v_cvt_pk_fp8_f32 rounds to nearest even (the
 // device format tests check it against the format definition on that range)
@@ -134,26 +135,29 @@ __device__ inline void fp4_setup(Fp4Group& G, float gmax, float c, float mn) {
   const _Float16 sh = (_Float16)sigma;
   G.s2 = f16x2{sh, sh};
   G.sum = 0.0f;
+  G.code[0] = G.code[1] = 0u;
+}
+// Weights of slots [I0, I1) (I0, I1 even): y = 2^(S c + off) from one exp2
+// each, added to the fp32 sum and converted to E2M1 in pairs right away.
+template <int I>
+__device__ inline void fp4_exp_pair(Fp4Group& G, const f32x16& S, float c) {
+  const float y0 = exp2_fast(__builtin_fmaf(S[I], c, G.off));
+  const float y1 = exp2_fast(__builtin_fmaf(S[I + 1], c, G.off));
+  G.sum += y0;
+  G.sum += y1;
+  G.code[I >> 3] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(G.code[I >> 3], y0, y1, 1.0f, (I >> 1) & 3);
 }
 template <int I0, int I1>
 __device__ inline void fp4_exps(Fp4Group& G, const f32x16& S, float c) {
-#pragma unroll
-  for (int i = I0; i < I1; ++i) {
-    G.y[i] = exp2_fast(__builtin_fmaf(S[i], c, G.off));
-    G.sum += G.y[i];
-  }
+  static_assert(I0 % 2 == 0 && I1 % 2 == 0, "whole pairs");
+  [&]<int... P>(std::integer_sequence<int, P...>) {
+    (fp4_exp_pair<I0 + 2 * P>(G, S, c), ...);
+  }(std::make_integer_sequence<int, (I1 - I0) / 2>{});
 }
+// sigma_P * E2M1 codes as fp16 pairs for the P^T operand (exact: at most 6
+// significant bits).
 __device__ inline void fp4_pack(const Fp4Group& G, f16x8& lo, f16x8& hi) {
-  const float* y = G.y;
-  // E2M1 codes, two per byte (byte selector must be a literal)
-  uint32_t f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
-  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, y[2], y[3], 1.0f, 1);
-  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, y[4], y[5], 1.0f, 2);
-  f0 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f0, y[6], y[7], 1.0f, 3);
-  uint32_t f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[8], y[9], 1.0f, 0);
-  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[10], y[11], 1.0f, 1);
-  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[12], y[13], 1.0f, 2);
-  f1 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(f1, y[14], y[15], 1.0f, 3);
+  const uint32_t f0 = G.code[0], f1 = G.code[1];
   const f16x2 s2 = G.s2;
   const f16x2 a0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 0) * s2;
   const f16x2 a1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(f0, 1.0f, 1) * s2;
@@ -333,6 +337,147 @@ __device__ inline void after(const T& v) {
   asm volatile("" ::"v"(v));
 }
 
+// ---- packed NVFP4 operands ---------------------------------------------------
+// Each block of a packed NVFP4 section holds 32 D bytes of E2M1 codes and 4 D
+// bytes of E4M3 group scales, ordered so that thread (wave w, lane l) of the
+// workgroup finds its share contiguous: D/16 code dwords at dword (w 64 + l) D/16
+// (dword i holds the 8 codes of one fp16 fragment, code e in nibble e), and
+// its scale bytes at 32 D + (w 32 + l%32) D/16 (Q, K: byte s scales fragment
+// s) or 32 D + (w 64 + l) D/32 (V: byte 2 t2 + h scales fragments (t2, 2h) and
+// (t2, 2h + 1)).
+template <int D>
+struct NvShare {
+  uint4 c[D / 64];  // D/16 code dwords
+  uint32_t s[(D / 16 + 3) / 4];  // scale bytes
+};
+
+template <int D>
+__device__ inline void nv_load_qk(NvShare<D>& x, const uint8_t* blk, int w, int lane) {
+  const uint4* c = reinterpret_cast<const uint4*>(blk + (w * 64 + lane) * (D / 4));
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) x.c[i] = c[i];
+  const uint8_t* sc = blk + 32 * D + (w * 32 + (lane & 31)) * (D / 16);
+  if constexpr (D == 128) {
+    const uint2 v = *reinterpret_cast<const uint2*>(sc);
+    x.s[0] = v.x;
+    x.s[1] = v.y;
+  } else {
+    x.s[0] = *reinterpret_cast<const uint32_t*>(sc);
+  }
+}
+template <int D>
+__device__ inline void nv_load_v(NvShare<D>& x, const uint8_t* blk, int w, int lane) {
+  const uint4* c = reinterpret_cast<const uint4*>(blk + (w * 64 + lane) * (D / 4));
+#pragma unroll
+  for (int i = 0; i < D / 64; ++i) x.c[i] = c[i];
+  const uint8_t* sc = blk + 32 * D + (w * 64 + lane) * (D / 32);
+  if constexpr (D == 128)
+    x.s[0] = *reinterpret_cast<const uint32_t*>(sc);
+  else
+    x.s[0] = *reinterpret_cast<const uint16_t*>(sc);
+}
+// fp16 fragment sigma * e of 8 codes (exact: at most 6 significant bits).
+__device__ inline f16x8 nv_frag(uint32_t codes, f16x2 s2) {
+  const f16x2 a0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, 0) * s2;
+  const f16x2 a1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, 1) * s2;
+  const f16x2 a2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, 2) * s2;
+  const f16x2 a3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(codes, 1.0f, 3) * s2;
+  return f16x8{a0[0], a0[1], a1[0], a1[1], a2[0], a2[1], a3[0], a3[1]};
+}
+// Exact fp16 values of scale bytes 2p and 2p + 1 of a share (E4M3 -> fp16 is exact).
+template <int D>
+__device__ inline f16x2 nv_scale_pair(const NvShare<D>& x, int p) {
+  return __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(x.s[p >> 1] >> (16 * (p & 1)), 1.0f, false);
+}
+// Fragment f of a Q or K share (f = s): codes dword f, scale byte f.
+template <int D>
+__device__ inline f16x8 nv_frag_qk(const NvShare<D>& x, int f) {
+  const f16x2 pr = nv_scale_pair(x, f >> 1);
+  const _Float16 sg = (f & 1) ? pr[1] : pr[0];
+  return nv_frag(x.c[f >> 2][f & 3], f16x2{sg, sg});
+}
+// Fragment f = 4 t2 + s of a V share: codes dword f, scale byte 2 t2 + s/2.
+template <int D>
+__device__ inline f16x8 nv_frag_v(const NvShare<D>& x, int f) {
+  const f16x2 pr = nv_scale_pair(x, f >> 2);
+  const _Float16 sg = ((f >> 1) & 1) ? pr[1] : pr[0];
+  return nv_frag(x.c[f >> 2][f & 3], f16x2{sg, sg});
+}
+
+// The NVFP4 phase's block loop. The key and value tiles of a block are decoded
+// from their packed sections into fp16 tiles in LDS by the two waves together
+// (each thread its own share), and read by both. Iteration i:
+//   region 1: S' = K(i+1) Q^T with the softmax of block i, and V(i) decoded
+//             into sV; then the packed V(i+1) is loaded
+//   -> barrier -> value product of block i with K(i+2) decoded into sK; then
+//   the packed K(i+3) is loaded -> barrier
+// Two barriers per block; each packed load has one iteration to arrive.
+// region1<MASK>(Sc, Sn, nb, vdec) calls vdec(f) once for each V fragment f;
+// pv(Sc, kdec) calls kdec(f) once for each K fragment f.
+template <int D, typename SA, typename FIRST, typename STEP1, typename PV>
+__device__ inline void nv_phase_loop(const uint16_t* list, int n, const int32_t* n_a, const float* dKh,
+                                     const uint8_t* Kh, const uint8_t* Vh, f16x8* sK, f16x8* sV, int wave, int lane,
+                                     FIRST first_qk, STEP1 region1, PV pv) {
+  constexpr int NB = nv_block_bytes(D);
+  constexpr int NS16 = D / 16;
+  NvShare<D> kx, vx;
+  KeyWin win = key_window(list, 0, n, n_a, dKh, lane);
+  auto block_at = [&](int e, int first) -> int {  // e - first < 128
+    return e - first < 64 ? lane_value(win.kb, e - first) : lane_value(win.kb_next, e - first - 64);
+  };
+  auto kdec = [&](int f) { sK[(wave * NS16 + f) * 64 + lane] = nv_frag_qk<D>(kx, f); };
+  auto vdec = [&](int f) { sV[(wave * NS16 + f) * 64 + lane] = nv_frag_v<D>(vx, f); };
+  // prologue: K(0) decoded and its logits computed, K(1) decoded, V(0) and K(2) loaded
+  const int kb0 = lane_value(win.kb, 0);
+  nv_load_qk<D>(kx, Kh + (int64_t)kb0 * NB, wave, lane);
+  nv_load_v<D>(vx, Vh + (int64_t)kb0 * NB, wave, lane);
+#pragma unroll
+  for (int f = 0; f < NS16; ++f) kdec(f);
+  wait_lds();
+  wg_barrier();
+  SA Sa, Sb;
+  first_qk(Sa);
+  if (n > 1) nv_load_qk<D>(kx, Kh + (int64_t)block_at(1, 0) * NB, wave, lane);
+  wait_lds();
+  wg_barrier();  // both waves have read K(0)
+  if (n > 1) {
+#pragma unroll
+    for (int f = 0; f < NS16; ++f) kdec(f);
+  }
+  if (n > 2) nv_load_qk<D>(kx, Kh + (int64_t)block_at(2, 0) * NB, wave, lane);
+  wait_lds();
+  wg_barrier();  // K(1) is in sK
+
+  auto step = [&](int it, SA& Sc, SA& Sn) {
+    const int first = it & ~63;
+    const int sl = it - first;
+    if (sl == 0 && it > 0) win = key_window(list, it, n, n_a, dKh, lane);
+    const int nb = lane_value(win.nb, sl);
+    const bool more1 = it + 1 < n, more3 = it + 3 < n;
+    const int kb1 = more1 ? block_at(it + 1, first) : 0;
+    const int kb3 = more3 ? block_at(it + 3, first) : 0;
+    // On the last block the logits of region 1 come from the unchanged tile and are not used.
+    if (nb < kCap)
+      region1.template operator()<true>(Sc, Sn, nb, vdec);
+    else
+      region1.template operator()<false>(Sc, Sn, nb, vdec);
+    if (more1) nv_load_v<D>(vx, Vh + (int64_t)kb1 * NB, wave, lane);
+    wait_lds();
+    wg_barrier();  // sV holds V(it); both waves are done with sK
+    // K(it+2) is decoded unconditionally: past the end of the list the share
+    // holds the previous block and the tile it writes is never read (one
+    // instantiation of pv keeps the register allocation of the loop small)
+    pv(Sc, kdec);
+    if (more3) nv_load_qk<D>(kx, Kh + (int64_t)kb3 * NB, wave, lane);
+    wait_lds();
+    wg_barrier();  // sK holds K(it+2); both waves are done with sV
+  };
+  for (int it = 0; it < n; it += 2) {
+    step(it, Sa, Sb);
+    if (it + 1 < n) step(it + 1, Sb, Sa);
+  }
+}
+
 // One precision phase of the block loop, software-pipelined by one block: the
 // logits of block i+1 are computed while the softmax of block i runs, so the
 // matrix cores and the vector ALUs work side by side inside each wave. The
@@ -440,6 +585,30 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
   const int bh = item / R, a = item % R;
   const Layout L = layout_view(args.layout, R, args.Npad);
   const int n4 = args.counts[4 * item], n8 = args.counts[4 * item + 1], n16 = args.counts[4 * item + 2];
+  // The operands must carry the tag of this layout version and fmt4, with the
+  // 16-bit sections when the row has 16-bit blocks; otherwise the row's
+  // output is zero and the mismatch is flagged in the lists meta area.
+  {
+    const uint32_t tag = __float_as_uint(args.g[(item / R) * 4 + 3]);
+    const uint32_t err = ((tag & ~0x1Fu) != (args.tag & ~0x1Fu) ? DA2_ATTN_ERR_LAYOUT : 0u) |
+                         ((tag & 0xFu) != (args.tag & 0xFu) ? DA2_ATTN_ERR_FMT4 : 0u) |
+                         (n16 > 0 && (!(tag & 0x10u) || !args.has16) ? DA2_ATTN_ERR_NO16 : 0u);
+    if (err) {
+      if (threadIdx.x == 0) atomicOr(reinterpret_cast<uint32_t*>(args.meta) + 1, err);
+      const Layout L0 = layout_view(args.layout, R, args.Npad);
+      const int nq0 = L0.n_a[item % R], b0 = (item / R) / args.H, h0 = (item / R) % args.H;
+      for (int i = threadIdx.x; i < nq0 * D; i += blockDim.x) {
+        const int q = i / D, c = i % D;
+        const int64_t o = (int64_t)b0 * args.ob + (int64_t)h0 * args.oh +
+                          (int64_t)L0.slot2tok[(int64_t)(item % R) * kCap + q] * args.on + c;
+        if (args.odtype == DA2_FP32)
+          reinterpret_cast<float*>(args.O)[o] = 0.0f;
+        else
+          reinterpret_cast<uint16_t*>(args.O)[o] = 0;
+      }
+      return;
+    }
+  }
   const uint16_t* keys = args.keys + (int64_t)item * R;
   const int64_t blk0 = (int64_t)bh * R;  // first block of this head
   const float* dKh = args.dK + blk0;
@@ -455,10 +624,14 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
   // ------------------------------ NVFP4 phase ------------------------------
   if (n4 > 0 && !mx) {
     const float c4 = args.g[bh * 4 + 0] * args.g[bh * 4 + 1] * kLog2e * rsqd;
+    // query fragments of this wave's tile, decoded once from the packed Q section
     f16x8 Qf[NS16];
-    const f16x8* Qa = reinterpret_cast<const f16x8*>(args.Q4) + (blk0 + a) * (kCap * D / 8);
+    {
+      NvShare<D> qx;
+      nv_load_qk<D>(qx, args.Q4 + (blk0 + a) * nv_block_bytes(D), qt, lane);
 #pragma unroll
-    for (int s = 0; s < NS16; ++s) Qf[s] = Qa[(qt * NS16 + s) * 64 + lane];
+      for (int s = 0; s < NS16; ++s) Qf[s] = nv_frag_qk<D>(qx, s);
+    }
     f16x8 P[4];
     float alpha = 1.0f;
     typedef f32x16 SA[2];
@@ -475,8 +648,9 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
     Fp4Group G0, G1;
     // Region 1: logits of the next block (NS16 stages of two MFMAs, operands
     // read one stage ahead) with the row maxima, the first group's weights and
-    // operands, and the second group's scale, in six pieces over the stages.
-    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float) {
+    // operands, the second group's scale (six pieces over the stages) and one
+    // value fragment decoded into sV per stage.
+    auto region1 = [&]<bool MASK, typename VDEC>(SA& Sc, SA& Sn, int nb, VDEC vdec) {
       if constexpr (MASK) mask_tail(Sc, nb, g);
       f16x8 k0 = sK[lane], k1 = sK[NS16 * 64 + lane];
       constexpr int NP = 6;
@@ -489,6 +663,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
         }
         Sn[0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(k0, Qf[s], s == 0 ? f32x16{} : Sn[0], 0, 0, 0);
         Sn[1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(k1, Qf[s], s == 0 ? f32x16{} : Sn[1], 0, 0, 0);
+        vdec(s);
 #pragma unroll
         for (int piece = 0; piece < NP; ++piece) {
           if (piece * NS16 / NP != s) continue;
@@ -499,9 +674,9 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
             mn = new_max(fmaxf(gm0, gm1), c4, m, l, alpha);
           } else if (piece == 2) {
             fp4_setup(G0, gm0, c4, mn);
-            fp4_exps<0, 5>(G0, Sc[0], c4);
+            fp4_exps<0, 6>(G0, Sc[0], c4);
           } else if (piece == 3) {
-            fp4_exps<5, 10>(G0, Sc[0], c4);
+            fp4_exps<6, 10>(G0, Sc[0], c4);
           } else if (piece == 4) {
             fp4_exps<10, 16>(G0, Sc[0], c4);
           } else {
@@ -514,13 +689,11 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
         k1 = n1;
       }
     };
-    // No separate region 2: the second group's weights are computed inside the
-    // value product, beside the MFMAs that use the first group's operands.
-    auto region2 = [&](SA&) {};
     // U += V^T P^T; value fragments are read two MFMAs ahead. The MFMAs of the
     // first group (k < 2 NT) carry the second group's exponentials and its
-    // fp16 operands, which the remaining MFMAs use.
-    auto pv = [&](SA& Sc) {
+    // fp16 operands, which the remaining MFMAs use; one key fragment of the
+    // block after next is decoded into sK every second MFMA.
+    auto pv = [&]<typename KDEC>(SA& Sc, KDEC kdec) {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
       constexpr int NM = 4 * NT;
       auto vfrag = [&](int k) { return sV[((k % NT) * 4 + k / NT) * 64 + lane]; };
@@ -545,12 +718,12 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
           fp4_pack(G1, P[2], P[3]);
           l += weight_sum(G0) + weight_sum(G1);
         }
+        if (k & 1) kdec(k >> 1);
         fence();
       }
     };
-    phase_loop<2 * NS16, f16x8, SA>(keys, n4, L.n_a, dKh, reinterpret_cast<const f16x8*>(args.K4) + blk0 * (kCap * D / 8),
-                                 reinterpret_cast<const f16x8*>(args.V4) + blk0 * (kCap * D / 8), sK, sV, wave, lane,
-                                 qk, region1, region2, pv);
+    nv_phase_loop<D, SA>(keys, n4, L.n_a, dKh, args.K4 + blk0 * nv_block_bytes(D), args.V4 + blk0 * nv_block_bytes(D),
+                         sK, sV, wave, lane, qk, region1, pv);
   }
 
   // ------------------------------ MXFP4 phase ------------------------------

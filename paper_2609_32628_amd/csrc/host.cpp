@@ -26,8 +26,8 @@ struct Dims {
 int32_t derive(const da2_problem* p, Dims* o) {
   if (!p) return DA2_ERR_INVALID_ARG;
   if (p->B <= 0 || p->H <= 0 || p->T <= 0 || p->Hg <= 0 || p->Wg <= 0 || p->d <= 0) return DA2_ERR_INVALID_ARG;
-  if (p->d != 64 && p->d != 128) return DA2_ERR_INVALID_ARG;
   if (p->partition != DA2_PART_TILES8 && p->partition != DA2_PART_RAGGED) return DA2_ERR_INVALID_ARG;
+  if (p->d != 64 && p->d != 128) return DA2_ERR_UNSUPPORTED;  // a valid head dim the kernels do not implement
   Dims d{};
   d.B = p->B;
   d.H = p->H;
@@ -53,7 +53,38 @@ inline int64_t mx_block_bytes(const Dims& d) { return 1024 * (d.d / 32 + 1); }
 
 constexpr int kSections = 16;
 
-void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
+// Byte size of each ops section (the index numbering of da2_ops_offsets).
+void section_sizes(const Dims& d, int64_t* sz) {
+  const int64_t e = d.BH * d.Npad * d.d;                       // values per operand
+  const int64_t nv = da2::nv_block_bytes((int)d.d) * d.BH * d.R;  // packed NVFP4 operand
+  const int64_t mx = mx_block_bytes(d) * d.BH * d.R;
+  const int64_t v[kSections] = {nv, nv, nv, e, e, e, 4 * d.BH * d.R, 4 * d.BH * d.R, 4 * d.BH * d.d, 16 * d.BH,
+                                2 * e, 2 * e, 2 * e, mx, mx, mx};
+  for (int i = 0; i < kSections; ++i) sz[i] = v[i];
+}
+
+// Offsets of the sections a run with (fmt4, with16) writes and reads, -1 for
+// the others: the 8-bit operands and all scales [3..9] first, then the 4-bit
+// encoding in use ([0..2] NVFP4 or [13..15] MXFP4), then the 16-bit operands
+// [10..12] when with16, so that no offset but the 16-bit ones depends on
+// with16. Returns the total size.
+int64_t ops_offsets(const Dims& d, int32_t fmt4, int32_t with16, int64_t* off) {
+  int64_t sz[kSections];
+  section_sizes(d, sz);
+  for (int i = 0; i < kSections; ++i) off[i] = -1;
+  const int nv[] = {3, 4, 5, 6, 7, 8, 9, 0, 1, 2, 10, 11, 12};
+  const int mx[] = {3, 4, 5, 6, 7, 8, 9, 13, 14, 15, 10, 11, 12};
+  const int* order = fmt4 == DA2_FMT4_MXFP4 ? mx : nv;
+  const int n = with16 ? 13 : 10;
+  int64_t o = 0;
+  for (int k = 0; k < n; ++k) {
+    off[order[k]] = o;
+    o += align_up(sz[order[k]]);
+  }
+  return o;
+}
+
+void sizes_of(const Dims& d, int32_t scope, int32_t fmt4, int32_t with16, da2_sizes_t* s) {
   std::memset(s, 0, sizeof(*s));
   s->R = (int32_t)d.R;
   s->Npad = (int32_t)d.Npad;
@@ -62,9 +93,8 @@ void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
   s->cls_bytes = d.BH * d.R * d.R;
   s->stats_bytes = 4 * d.BH * (4 + d.d);
   s->lists_bytes = align_up(2 * d.BH * d.R * d.R) + align_up(16 * d.BH * d.R) + align_up(4 * d.BH * d.R) + kAlign;
-  const int64_t e = d.BH * d.Npad * d.d;
-  s->ops_bytes = 3 * align_up(2 * e) + 3 * align_up(e) + 2 * align_up(4 * d.BH * d.R) + align_up(4 * d.BH * d.d) +
-                 align_up(16 * d.BH) + 3 * align_up(2 * e) + 3 * align_up(mx_block_bytes(d) * d.BH * d.R);
+  int64_t off[kSections];
+  s->ops_bytes = ops_offsets(d, fmt4, with16, off);
   s->ws_draft_bytes = 4 * align_up(8 * d.BH * d.R * d.d) + 2 * align_up(8 * d.BH * d.R * d.R) + align_up(8 * d.BH * d.R);
   int64_t thr = scope == DA2_SCOPE_ROW ? 8 * da2::kCuts * d.BH * d.R : 8 * da2::kCuts * d.BH;
   s->ws_rank_bytes = align_up(4 * d.BH * da2::kCuts * 2048) + align_up(thr) + align_up(8 * da2::kCuts * d.BH) +
@@ -73,16 +103,8 @@ void sizes_of(const Dims& d, int32_t scope, da2_sizes_t* s) {
   s->ws_prep_bytes = 0;
 }
 
-void ops_offsets(const Dims& d, int64_t* off) {
-  const int64_t e = d.BH * d.Npad * d.d;
-  int64_t o = 0;
-  const int64_t mx = mx_block_bytes(d) * d.BH * d.R;
-  const int64_t sz[kSections] = {2 * e, 2 * e, 2 * e, e, e, e, 4 * d.BH * d.R, 4 * d.BH * d.R, 4 * d.BH * d.d,
-                                 16 * d.BH, 2 * e, 2 * e, 2 * e, mx, mx, mx};
-  for (int i = 0; i < kSections; ++i) {
-    off[i] = o;
-    o += align_up(sz[i]);
-  }
+bool fmt_ok(int32_t fmt4, int32_t with16) {
+  return (fmt4 == DA2_FMT4_NVFP4 || fmt4 == DA2_FMT4_MXFP4) && (with16 == 0 || with16 == 1);
 }
 
 void lists_offsets(const Dims& d, int64_t* off) {
@@ -197,14 +219,16 @@ const char* da2_status_string(int32_t s) {
   }
 }
 
-int32_t da2_sizes(const da2_problem* p, int32_t scope, da2_sizes_t* out) {
+int32_t da2_sizes(const da2_problem* p, int32_t scope, int32_t fmt4, int32_t with16, da2_sizes_t* out) {
   Dims d;
   int32_t st = derive(p, &d);
   if (st) return st;
-  if (!out || (scope != DA2_SCOPE_HEAD && scope != DA2_SCOPE_ROW)) return DA2_ERR_INVALID_ARG;
-  sizes_of(d, scope, out);
+  if (!out || (scope != DA2_SCOPE_HEAD && scope != DA2_SCOPE_ROW) || !fmt_ok(fmt4, with16)) return DA2_ERR_INVALID_ARG;
+  sizes_of(d, scope, fmt4, with16, out);
   return DA2_OK;
 }
+
+int32_t da2_ops_layout_version(void) { return DA2_OPS_LAYOUT_VERSION; }
 
 int32_t da2_ws_draft_offsets(const da2_problem* p, int64_t* off) {
   Dims d;
@@ -224,12 +248,12 @@ int32_t da2_lists_offsets(const da2_problem* p, int64_t* off) {
   return DA2_OK;
 }
 
-int32_t da2_ops_offsets(const da2_problem* p, int64_t* off) {
+int32_t da2_ops_offsets(const da2_problem* p, int32_t fmt4, int32_t with16, int64_t* off) {
   Dims d;
   int32_t st = derive(p, &d);
   if (st) return st;
-  if (!off) return DA2_ERR_INVALID_ARG;
-  ops_offsets(d, off);
+  if (!off || !fmt_ok(fmt4, with16)) return DA2_ERR_INVALID_ARG;
+  ops_offsets(d, fmt4, with16, off);
   return DA2_OK;
 }
 
@@ -276,7 +300,7 @@ int32_t da2_draft_map(const void* Q, const void* K, const da2_tensor* qk, const 
   if (!aligned16(Q) || !aligned16(K)) return DA2_ERR_INVALID_ARG;
   if (!(lambda >= 0.0 && lambda <= 1.0)) return DA2_ERR_INVALID_ARG;
   da2_sizes_t sz;
-  sizes_of(d, DA2_SCOPE_HEAD, &sz);
+  sizes_of(d, DA2_SCOPE_HEAD, DA2_FMT4_NVFP4, 0, &sz);
   if (ws_bytes < sz.ws_draft_bytes) return DA2_ERR_WORKSPACE;
   if ((st = check_device())) return st;
   int64_t off[7];
@@ -381,7 +405,7 @@ int32_t da2_rank_assign(const float* A, const da2_problem* p, int32_t num16, int
   if (st) return st;
   if (!ws) return DA2_ERR_INVALID_ARG;
   da2_sizes_t sz;
-  sizes_of(d, scope, &sz);
+  sizes_of(d, scope, DA2_FMT4_NVFP4, 0, &sz);
   if (ws_bytes < sz.ws_rank_bytes) return DA2_ERR_WORKSPACE;
   if ((st = check_device())) return st;
   return rank_launch(A, d, num16, num8, num4, den, scope, cls, lists, ws, stream);
@@ -393,7 +417,7 @@ int32_t da2_rank_assign_noalloc(const float* A, const da2_problem* p, int32_t nu
   int32_t st = rank_check(A, p, num16, num8, num4, den, scope, cls, lists, &d);
   if (st) return st;
   da2_sizes_t sz;
-  sizes_of(d, scope, &sz);
+  sizes_of(d, scope, DA2_FMT4_NVFP4, 0, &sz);
   static_assert(da2::kRankScratchBytes == DA2_RANK_NOALLOC_MAX_BYTES, "header limit and scratch size agree");
   if (sz.ws_rank_bytes > da2::kRankScratchBytes) return DA2_ERR_WORKSPACE;
   if ((st = check_device())) return st;
@@ -403,22 +427,23 @@ int32_t da2_rank_assign_noalloc(const float* A, const da2_problem* p, int32_t nu
 }
 
 int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2_tensor* qkv, const int32_t* layout,
-                          const da2_problem* p, int32_t with16, int32_t fmt4, void* stats, void* ops, void* ws,
-                          int64_t ws_bytes, void* stream) {
+                          const da2_problem* p, int32_t with16, int32_t fmt4, void* stats, void* ops,
+                          int64_t ops_bytes, void* ws, int64_t ws_bytes, void* stream) {
   Dims d;
   int32_t st = derive(p, &d);
   if (st) return st;
   if ((st = check_tensor(qkv, d, false))) return st;
   if (!Q || !K || !V || !layout || !stats || !ops) return DA2_ERR_INVALID_ARG;
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V)) return DA2_ERR_INVALID_ARG;
-  if (with16 != 0 && with16 != 1) return DA2_ERR_INVALID_ARG;
-  if (fmt4 != DA2_FMT4_NVFP4 && fmt4 != DA2_FMT4_MXFP4) return DA2_ERR_INVALID_ARG;
+  if (!fmt_ok(fmt4, with16)) return DA2_ERR_INVALID_ARG;
   (void)ws;
   if (ws_bytes < 0) return DA2_ERR_WORKSPACE;
-  if ((st = check_device())) return st;
   int64_t off[kSections];
-  ops_offsets(d, off);
+  if (ops_bytes < ops_offsets(d, fmt4, with16, off)) return DA2_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
   char* ob = static_cast<char*>(ops);
+  // sections this run does not write get no pointer (the kernels skip them)
+  auto sec = [&](int i) -> char* { return off[i] < 0 ? nullptr : ob + off[i]; };
   da2::PrepArgs a{};
   a.with16 = with16;
   a.fmt4 = fmt4;
@@ -437,56 +462,68 @@ int32_t da2_prep_operands(const void* Q, const void* K, const void* V, const da2
   a.N = (int)d.N;
   a.layout = layout;
   a.stats = static_cast<uint32_t*>(stats);
-  a.Q4 = reinterpret_cast<_Float16*>(ob + off[0]);
-  a.K4 = reinterpret_cast<_Float16*>(ob + off[1]);
-  a.V4 = reinterpret_cast<_Float16*>(ob + off[2]);
-  a.Q8 = reinterpret_cast<int8_t*>(ob + off[3]);
-  a.K8 = reinterpret_cast<int8_t*>(ob + off[4]);
-  a.V8 = reinterpret_cast<uint8_t*>(ob + off[5]);
-  a.dQ = reinterpret_cast<float*>(ob + off[6]);
-  a.dK = reinterpret_cast<float*>(ob + off[7]);
-  a.dV = reinterpret_cast<float*>(ob + off[8]);
-  a.g = reinterpret_cast<float*>(ob + off[9]);
-  a.Q16 = reinterpret_cast<_Float16*>(ob + off[10]);
-  a.K16 = reinterpret_cast<_Float16*>(ob + off[11]);
-  a.V16 = reinterpret_cast<_Float16*>(ob + off[12]);
-  a.Q4mx = reinterpret_cast<uint8_t*>(ob + off[13]);
-  a.K4mx = reinterpret_cast<uint8_t*>(ob + off[14]);
-  a.V4mx = reinterpret_cast<uint8_t*>(ob + off[15]);
+  a.Q4 = reinterpret_cast<uint8_t*>(sec(0));
+  a.K4 = reinterpret_cast<uint8_t*>(sec(1));
+  a.V4 = reinterpret_cast<uint8_t*>(sec(2));
+  a.Q8 = reinterpret_cast<int8_t*>(sec(3));
+  a.K8 = reinterpret_cast<int8_t*>(sec(4));
+  a.V8 = reinterpret_cast<uint8_t*>(sec(5));
+  a.dQ = reinterpret_cast<float*>(sec(6));
+  a.dK = reinterpret_cast<float*>(sec(7));
+  a.dV = reinterpret_cast<float*>(sec(8));
+  a.g = reinterpret_cast<float*>(sec(9));
+  a.Q16 = reinterpret_cast<_Float16*>(sec(10));
+  a.K16 = reinterpret_cast<_Float16*>(sec(11));
+  a.V16 = reinterpret_cast<_Float16*>(sec(12));
+  a.Q4mx = reinterpret_cast<uint8_t*>(sec(13));
+  a.K4mx = reinterpret_cast<uint8_t*>(sec(14));
+  a.V4mx = reinterpret_cast<uint8_t*>(sec(15));
+  a.tag = da2::ops_tag(fmt4, with16);
   return hip_status(da2::launch_prep(a, static_cast<hipStream_t>(stream)));
 }
 
-int32_t da2_mixed_attn(const void* ops, const void* lists, const int32_t* layout, const da2_problem* p, int32_t fmt4,
-                       const da2_tensor* out, void* O, void* stream) {
+int32_t da2_mixed_attn(const void* ops, int64_t ops_bytes, const void* lists, const int32_t* layout,
+                       const da2_problem* p, int32_t fmt4, const da2_tensor* out, void* O, void* stream) {
   Dims d;
   int32_t st = derive(p, &d);
   if (st) return st;
   if ((st = check_tensor(out, d, true))) return st;
   if (!ops || !lists || !layout || !O) return DA2_ERR_INVALID_ARG;
   if (fmt4 != DA2_FMT4_NVFP4 && fmt4 != DA2_FMT4_MXFP4) return DA2_ERR_INVALID_ARG;
-  if ((st = check_device())) return st;
   int64_t off[kSections], lo[4];
-  ops_offsets(d, off);
+  // at least the sections of a run without the 16-bit path; the 16-bit
+  // sections are read only when the buffer holds them too
+  if (ops_bytes < ops_offsets(d, fmt4, 0, off)) return DA2_ERR_INVALID_ARG;
+  const bool has16 = ops_bytes >= ops_offsets(d, fmt4, 1, off);
+  if ((st = check_device())) return st;
+  // the 16-bit sections come last, so the other offsets do not depend on
+  // with16; the kernel reads the 16-bit ones only when a row holds 16-bit
+  // blocks and the operands' tag says they were written
+  ops_offsets(d, fmt4, 1, off);
   lists_offsets(d, lo);
   const char* ob = static_cast<const char*>(ops);
+  auto sec = [&](int i) -> const char* { return off[i] < 0 ? nullptr : ob + off[i]; };
   const char* lb = static_cast<const char*>(lists);
   da2::AttnArgs a{};
-  a.Q4 = reinterpret_cast<const _Float16*>(ob + off[0]);
-  a.K4 = reinterpret_cast<const _Float16*>(ob + off[1]);
-  a.V4 = reinterpret_cast<const _Float16*>(ob + off[2]);
-  a.Q8 = reinterpret_cast<const int8_t*>(ob + off[3]);
-  a.K8 = reinterpret_cast<const int8_t*>(ob + off[4]);
-  a.V8 = reinterpret_cast<const uint8_t*>(ob + off[5]);
-  a.dQ = reinterpret_cast<const float*>(ob + off[6]);
-  a.dK = reinterpret_cast<const float*>(ob + off[7]);
-  a.dV = reinterpret_cast<const float*>(ob + off[8]);
-  a.g = reinterpret_cast<const float*>(ob + off[9]);
-  a.Q16 = reinterpret_cast<const _Float16*>(ob + off[10]);
-  a.K16 = reinterpret_cast<const _Float16*>(ob + off[11]);
-  a.V16 = reinterpret_cast<const _Float16*>(ob + off[12]);
-  a.Q4mx = reinterpret_cast<const uint8_t*>(ob + off[13]);
-  a.K4mx = reinterpret_cast<const uint8_t*>(ob + off[14]);
-  a.V4mx = reinterpret_cast<const uint8_t*>(ob + off[15]);
+  a.Q4 = reinterpret_cast<const uint8_t*>(sec(0));
+  a.K4 = reinterpret_cast<const uint8_t*>(sec(1));
+  a.V4 = reinterpret_cast<const uint8_t*>(sec(2));
+  a.Q8 = reinterpret_cast<const int8_t*>(sec(3));
+  a.K8 = reinterpret_cast<const int8_t*>(sec(4));
+  a.V8 = reinterpret_cast<const uint8_t*>(sec(5));
+  a.dQ = reinterpret_cast<const float*>(sec(6));
+  a.dK = reinterpret_cast<const float*>(sec(7));
+  a.dV = reinterpret_cast<const float*>(sec(8));
+  a.g = reinterpret_cast<const float*>(sec(9));
+  a.Q16 = reinterpret_cast<const _Float16*>(sec(10));
+  a.K16 = reinterpret_cast<const _Float16*>(sec(11));
+  a.V16 = reinterpret_cast<const _Float16*>(sec(12));
+  a.Q4mx = reinterpret_cast<const uint8_t*>(sec(13));
+  a.K4mx = reinterpret_cast<const uint8_t*>(sec(14));
+  a.V4mx = reinterpret_cast<const uint8_t*>(sec(15));
+  a.tag = da2::ops_tag(fmt4, 0);
+  a.has16 = has16 ? 1 : 0;
+  a.meta = reinterpret_cast<int32_t*>(const_cast<char*>(lb) + lo[3]);
   a.fmt4 = fmt4;
   a.keys = reinterpret_cast<const uint16_t*>(lb + lo[0]);
   a.counts = reinterpret_cast<const int32_t*>(lb + lo[1]);

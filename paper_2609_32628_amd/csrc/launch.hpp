@@ -5,7 +5,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/da2.h"
+
 namespace da2 {
+
+// Bytes of one block (64 slots x D channels) of a packed NVFP4 section: the
+// E2M1 codes (4 bits per value) and one E4M3 scale byte per 16 values.
+constexpr int nv_block_bytes(int D) { return 32 * D + 4 * D; }
 
 struct DraftArgs {
   const void* Q;
@@ -55,7 +61,7 @@ struct PrepArgs {
   const int32_t* layout;
   uint32_t* stats;
   // ops sections
-  _Float16 *Q4, *K4, *V4;
+  uint8_t *Q4, *K4, *V4;  // packed NVFP4 (codes and E4M3 scales)
   int8_t *Q8, *K8;
   uint8_t* V8;
   float *dQ, *dK, *dV, *g;
@@ -63,16 +69,20 @@ struct PrepArgs {
   uint8_t *Q4mx, *K4mx, *V4mx;  // MXFP4 operands (written instead of Q4/K4/V4 when fmt4 = MXFP4)
   int with16;
   int fmt4;
+  uint32_t tag;  // ops_tag(fmt4, with16), written into word 3 of each head's g entry
 };
 
 struct AttnArgs {
-  const _Float16 *Q4, *K4, *V4;
+  const uint8_t *Q4, *K4, *V4;  // packed NVFP4 (codes and E4M3 scales)
   const int8_t *Q8, *K8;
   const uint8_t* V8;
   const float *dQ, *dK, *dV, *g;
   const _Float16 *Q16, *K16, *V16;
   const uint8_t *Q4mx, *K4mx, *V4mx;
   int fmt4;
+  uint32_t tag;   // ops_tag(fmt4, 0): expected tag of the operands (the with16 bit is checked per row)
+  int has16;      // the ops buffer is large enough to hold the 16-bit sections
+  int32_t* meta;  // lists meta area: word 1 collects the error flags of a mismatch
   const uint16_t* keys;
   const int32_t* counts;
   const int32_t* order;
@@ -88,6 +98,15 @@ struct AttnArgs {
 constexpr int64_t kRankScratchBytes = 8ll << 20;
 // Device address of the current device's scratch array (looked up once per device).
 hipError_t rank_scratch_address(void** out);
+
+// Tag that da2_prep_operands writes into word 3 of each head's g entry and
+// da2_mixed_attn checks: a fixed marker, the ops layout version, with16 (bit
+// 4) and fmt4 (bits 0..3).
+constexpr uint32_t kTagMarker = 0xDA200000u;
+constexpr uint32_t ops_tag(int fmt4, int with16) {
+  return kTagMarker | (static_cast<uint32_t>(DA2_OPS_LAYOUT_VERSION) << 8) | (with16 ? 0x10u : 0u) |
+         static_cast<uint32_t>(fmt4);
+}
 
 hipError_t launch_draft(const DraftArgs& args, hipStream_t stream);
 hipError_t launch_rank(const RankArgs& args, hipStream_t stream);

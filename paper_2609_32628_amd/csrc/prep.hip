@@ -14,10 +14,11 @@
 // Every encoding is written in the MFMA fragment order of the attention kernel
 // (16-byte chunks, one per lane of a fragment):
 //   INT8 Q, K with per-block scales, E4M3 V with per-channel scales,
-//   NVFP4 Q, K (16-channel groups) and V (16-slot groups) as the exact fp16
-//   value sigma*e,
+//   NVFP4 Q, K (16-channel groups) and V (16-slot groups) as E2M1 codes with
+//   one E4M3 scale byte per group, ordered by the attention thread that
+//   decodes them (the per-head tensor scales and an encoding tag go to g),
 //   and, when asked for, the half-precision Q, K, V of the 16-bit path in the
-//   same fragment order as the NVFP4 sections;
+//   fp16 fragment order the NVFP4 codes decode to;
 //   with the MXFP4 encoding instead of NVFP4: E2M1 codes of 32-element blocks
 //   (channels for Q and K, key slots for V) with E8M0 scale words, in the
 //   operand order of the scaled fp4 MFMA.
@@ -133,40 +134,36 @@ __device__ inline uint4 int8_codes16(const float* x, float inv) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// sigma * E2M1(y) for 8 scaled values y, as fp16 (exact; an E2M1 zero keeps
-// the sign of y, as the hardware cast does).
-__device__ inline uint4 nvfp4_values8(const float* y, f16x2 s2) {
+// ---- MXFP4 / NVFP4 codes --------------------------------------------------------
+// E2M1 codes of 8 values, value e in nibble e (low nibble first).
+__device__ inline uint32_t fp4_codes8(const float* y) {
   uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
   c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[2], y[3], 1.0f, 1);
   c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[4], y[5], 1.0f, 2);
-  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[6], y[7], 1.0f, 3);
-  const f16x2 d0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 0) * s2;
-  const f16x2 d1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 1) * s2;
-  const f16x2 d2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 2) * s2;
-  const f16x2 d3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(c, 1.0f, 3) * s2;
-  return make_uint4(__builtin_bit_cast(uint32_t, d0), __builtin_bit_cast(uint32_t, d1),
-                    __builtin_bit_cast(uint32_t, d2), __builtin_bit_cast(uint32_t, d3));
+  return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[6], y[7], 1.0f, 3);
 }
 
-// NVFP4 encoding of one 16-element group x with tensor scale gX (sixg = f32(6 gX)):
-// the two fp16 chunks of elements [0,8) and [8,16).
-__device__ inline void nvfp4_group16(const float* x, float gX, float sixg, uint4& lo, uint4& hi) {
+// NVFP4 encoding of one 16-element group x with tensor scale gX (sixg =
+// f32(6 gX)): the E2M1 codes of elements [0,8) and [8,16) (value e in nibble
+// e) and the E4M3 code of the group scale sigma (a zero sigma gives zero codes;
+// an E2M1 zero keeps the sign of its scaled value, as the hardware cast does).
+__device__ inline void nvfp4_group16(const float* x, float gX, float sixg, uint32_t& lo, uint32_t& hi,
+                                     uint32_t& scode) {
   float gm = 0.0f;
 #pragma unroll
   for (int e = 0; e < 16; ++e) gm = fmaxf(gm, fabsf(x[e]));
   const float sigma = e4m3_round_mag(__fdiv_rn(gm, sixg));
   if (sigma == 0.0f) {
-    lo = hi = make_uint4(0u, 0u, 0u, 0u);
+    lo = hi = scode = 0u;
     return;
   }
   const float inv = __fdiv_rn(1.0f, __fmul_rn(gX, sigma));
   float y[16];
 #pragma unroll
   for (int e = 0; e < 16; ++e) y[e] = __fmul_rn(x[e], inv);
-  const _Float16 sh = (_Float16)sigma;
-  const f16x2 s2 = {sh, sh};
-  lo = nvfp4_values8(y, s2);
-  hi = nvfp4_values8(y + 8, s2);
+  lo = fp4_codes8(y);
+  hi = fp4_codes8(y + 8);
+  scode = e4m3_code(sigma);  // sigma is an E4M3 value: its exact code
 }
 
 // ---- MXFP4 --------------------------------------------------------------------
@@ -176,13 +173,6 @@ __device__ inline void nvfp4_group16(const float* x, float gX, float sixg, uint4
 __device__ inline int mx_exponent(float amax) { return max((int)(__float_as_uint(amax) >> 23) - 129, -127); }
 // 2^-k as a float (normal for every k from mx_exponent).
 __device__ inline float mx_inv_scale(int k) { return __uint_as_float(static_cast<uint32_t>(127 - k) << 23); }
-// E2M1 codes of 8 values, value e in nibble e (low nibble first).
-__device__ inline uint32_t fp4_codes8(const float* y) {
-  uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
-  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[2], y[3], 1.0f, 1);
-  c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[4], y[5], 1.0f, 2);
-  return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y[6], y[7], 1.0f, 3);
-}
 // MXFP4 sections: bytes per block (d/32 data fragments and the scale fragment).
 constexpr int mx_block_bytes(int D) { return 1024 * (D / 32 + 1); }
 
@@ -243,7 +233,7 @@ __global__ __launch_bounds__(256) void prep_qk_kernel(PrepArgs args) {
   const float gX = nvfp4_scale_global(args.stats[(int64_t)bh * (4 + D) + which]);
   const float sixg = __fmul_rn(6.0f, gX);
   int8_t* out8 = (which == 0 ? args.Q8 : args.K8) + blk * (int64_t)kCap * D;
-  _Float16* out4 = (which == 0 ? args.Q4 : args.K4) + blk * (int64_t)kCap * D;
+  uint8_t* out4 = (which == 0 ? args.Q4 : args.K4) + blk * (int64_t)nv_block_bytes(D);
 #pragma unroll
   for (int k = 0; k < UPT; ++k) {
     const int u = tid + 256 * k, c16 = u % NG, rr = u / NG;
@@ -251,13 +241,16 @@ __global__ __launch_bounds__(256) void prep_qk_kernel(PrepArgs args) {
     // INT8 chunk: [jq][c16/2][lane = r + 32 (c16%2)][16]
     const int64_t c8 = ((int64_t)(jq * NS32 + (c16 >> 1)) * 64 + r + 32 * (c16 & 1)) * 16;
     *reinterpret_cast<uint4*>(out8 + c8) = int8_codes16(x[k], inv8);
-    // NVFP4 chunks: [jq][c16][lane = r + 32 g][8] for halves g = 0, 1
+    // fp16 chunks of the 16-bit path: [jq][c16][lane = r + 32 g][8] for halves g = 0, 1
     const int64_t c4 = ((int64_t)(jq * NG + c16) * 64 + r) * 8;
     if (args.fmt4 == DA2_FMT4_NVFP4) {
-      uint4 lo, hi;
-      nvfp4_group16(x[k], gX, sixg, lo, hi);
-      *reinterpret_cast<uint4*>(out4 + c4) = lo;
-      *reinterpret_cast<uint4*>(out4 + c4 + 32 * 8) = hi;
+      // packed NVFP4: the codes of elements 8g + [0, 8) are dword c16 of lane
+      // r + 32 g of tile jq; the scale is byte c16 of row r of tile jq
+      uint32_t lo, hi, sc;
+      nvfp4_group16(x[k], gX, sixg, lo, hi, sc);
+      *reinterpret_cast<uint32_t*>(out4 + ((int64_t)(jq * 64 + r) * NG + c16) * 4) = lo;
+      *reinterpret_cast<uint32_t*>(out4 + ((int64_t)(jq * 64 + r + 32) * NG + c16) * 4) = hi;
+      out4[32 * D + (jq * 32 + r) * NG + c16] = static_cast<uint8_t>(sc);
     } else {
       // MXFP4: the 32-channel block is this group and its neighbour c16 ^ 1,
       // held by the adjacent lane. The group's 16 codes are half of a lane's
@@ -365,13 +358,20 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
         code = make_uint4(w[0], w[1], w[2], w[3]);
       }
       *reinterpret_cast<uint4*>(args.V8 + blk * (int64_t)kCap * D + ((int64_t)(2 * t + (sg >> 1)) * 64 + lane) * 16) = code;
-      // NVFP4 along slots: chunks [t][s = 2 (sg/2) + half][lane][8]
+      // fp16 chunks of the 16-bit path: [t][s = 2 (sg/2) + half][lane][8]
       const int64_t c4 = blk * (int64_t)kCap * D + ((int64_t)(4 * t + 2 * (sg >> 1)) * 64 + lane) * 8;
       if (args.fmt4 == DA2_FMT4_NVFP4) {
-        uint4 lo, hi;
-        nvfp4_group16(xc, gV, sixg, lo, hi);
-        *reinterpret_cast<uint4*>(args.V4 + c4) = lo;
-        *reinterpret_cast<uint4*>(args.V4 + c4 + 64 * 8) = hi;
+        // packed NVFP4 along slots: channel tile t = w NT/2 + t2 belongs to
+        // attention wave w; the codes of fragments s = 2 (sg/2) and 2 (sg/2) + 1
+        // are dwords s of the lane's tile t2, the scale is byte h = sg/2
+        constexpr int NTH = D / 64;  // channel tiles per wave
+        const int w = t / NTH, t2 = t % NTH;
+        uint32_t lo, hi, sc;
+        nvfp4_group16(xc, gV, sixg, lo, hi, sc);
+        uint8_t* base = args.V4 + blk * (int64_t)nv_block_bytes(D);
+        *reinterpret_cast<uint2*>(base + ((int64_t)((w * 64 + lane) * NTH + t2) * 4 + 2 * (sg >> 1)) * 4) =
+            make_uint2(lo, hi);
+        base[32 * D + ((w * 64 + lane) * NTH + t2) * 2 + (sg >> 1)] = static_cast<uint8_t>(sc);
       }
       if (args.with16) {  // 16-bit path: the same chunks as fp16(v)
         *reinterpret_cast<uint4*>(args.V16 + c4) = half8(xc);
@@ -412,7 +412,7 @@ __global__ __launch_bounds__(256) void prep_v_kernel(PrepArgs args) {
   }
   if (a == 0) {
     if (tid < D) args.dV[(int64_t)bh * D + tid] = __fdiv_rn(__uint_as_float(st[4 + tid]), 2.25f);
-    if (tid < 4) args.g[(int64_t)bh * 4 + tid] = tid < 3 ? nvfp4_scale_global(st[tid]) : 0.0f;
+    if (tid < 4) args.g[(int64_t)bh * 4 + tid] = tid < 3 ? nvfp4_scale_global(st[tid]) : __uint_as_float(args.tag);
   }
 }
 

@@ -421,7 +421,10 @@ __global__ __launch_bounds__(1024) void rank_order_kernel(RankArgs args) {
     const uint32_t pos = atomicAdd(&hist[order_key(args, i)], 1u);
     args.order[pos] = (int32_t)i;
   }
-  if (threadIdx.x == 0) args.meta[0] = (int32_t)n;
+  if (threadIdx.x == 0) {
+    args.meta[0] = (int32_t)n;
+    args.meta[1] = 0;  // error flags of da2_mixed_attn calls on these lists
+  }
 }
 
 // Fixed device scratch for callers that cannot allocate (da2_rank_assign_noalloc):

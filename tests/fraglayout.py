@@ -89,7 +89,7 @@ def index_mx_v(d):
 
 
 def _pack_nibbles(codes):
-    """[..., 32] 4-bit codes -> [..., 16] bytes, code 2b in the low nibble of byte b."""
+    """[..., 2n] 4-bit codes -> [..., n] bytes, code 2b in the low nibble of byte b."""
     c = codes.astype(np.uint8)
     return (c[..., 0::2] & 0xF) | ((c[..., 1::2] & 0xF) << 4)
 
@@ -120,14 +120,49 @@ def mx_section(kind, codes, kexp):
     return frags.reshape(R, -1)
 
 
+def nv_section(kind, codes, scodes):
+    """Bytes [R, 36 d] of a packed NVFP4 section.
+
+    kind "Q", "K": codes [R, 64, d] E2M1 codes (slot ordered), scodes
+    [R, 64, d/16] E4M3 codes of the (slot, 16-channel group) scales; kind
+    "V": codes [R, 64, d], scodes [R, 4, d] E4M3 codes of the (16-slot group,
+    channel) scales. The order is that of include/da2.h: per attention thread
+    (wave w, lane) its code dwords, then the scale bytes."""
+    R, _, d = codes.shape
+    ns, nt = d // 16, d // 32
+    r, g = _lanes()
+    if kind in ("Q", "K"):
+        slot, ch = index_q4(d, kind == "K")                           # [2, ns, 64, 8]
+        frag = codes[:, slot, ch]                                     # [R, 2, ns, 64, 8]
+        frag = frag.transpose(0, 1, 3, 2, 4)                          # [R, w, lane, s, 8]
+        code_bytes = _pack_nibbles(frag).reshape(R, -1)                 # 32 d bytes
+        w = np.arange(2)[:, None, None]
+        rr = np.arange(32)[None, :, None]
+        sg = np.arange(ns)[None, None, :]
+        row = kappa(w, rr) if kind == "K" else 32 * w + rr
+        scale_bytes = scodes[:, row, sg].reshape(R, -1)               # [R, 2*32*ns]
+    else:
+        slot, ch = index_v4(d)                                        # [nt, 4, 64, 8]
+        frag = codes[:, slot, ch].reshape(R, 2, nt // 2, 4, 64, 8)    # [R, w, t2, s, lane, 8]
+        frag = frag.transpose(0, 1, 4, 2, 3, 5)                       # [R, w, lane, t2, s, 8]
+        code_bytes = _pack_nibbles(frag).reshape(R, -1)
+        w = np.arange(2)[:, None, None, None]
+        lane = np.arange(64)[None, :, None, None]
+        t2 = np.arange(nt // 2)[None, None, :, None]
+        h = np.arange(2)[None, None, None, :]
+        t = w * (nt // 2) + t2
+        kg = 2 * h + lane // 32
+        scale_bytes = scodes[:, kg, 32 * t + lane % 32].reshape(R, -1)  # [R, 2*64*(nt/2)*2]
+    out = np.concatenate([code_bytes, scale_bytes], axis=1).astype(np.uint8)
+    assert out.shape[1] == 36 * d
+    return out
+
+
 SECTIONS = {
-    "Q4": (lambda d: index_q4(d, False), np.float16),
-    "K4": (lambda d: index_q4(d, True), np.float16),
-    "V4": (index_v4, np.float16),
     "Q8": (lambda d: index_q8(d, False), np.int8),
     "K8": (lambda d: index_q8(d, True), np.int8),
     "V8": (index_v8, np.uint8),
-    "Q16": (lambda d: index_q4(d, False), np.float16),   # 16-bit path: the Q4 / K4 / V4 layouts
+    "Q16": (lambda d: index_q4(d, False), np.float16),   # 16-bit path: the fp16 fragment orders
     "K16": (lambda d: index_q4(d, True), np.float16),
     "V16": (index_v4, np.float16),
 }

@@ -8,9 +8,9 @@ import numpy as np
 import torch
 
 from oracle import encode, formats, partition, pipeline, rank
-from paper_2609_32628_amd import api
+from paper_2609_32628_amd import _lib, api
 from synth import configs, gen
-from fraglayout import mx_section, to_frag
+from fraglayout import mx_section, nv_section, to_frag
 
 TOL_MAX_ABS = 2e-2     # output tolerances of the parity bar
 TOL_REL_L2 = 5e-3
@@ -40,19 +40,37 @@ def to_device(X, w):
     return t.to(torch.bfloat16 if w.dtype == "bf16" else torch.float32).cuda()
 
 
+SECTION_NAMES = ["Q4", "K4", "V4", "Q8", "K8", "V8", "dQ", "dK", "dV", "g", "Q16", "K16", "V16",
+                 "Q4mx", "K4mx", "V4mx"]
+
+
+def section_specs(p, R):
+    """(dtype, per-head shape) of each ops section, in da2_ops_offsets order."""
+    d = p.d
+    mx = (d // 32 + 1) * 1024
+    return [(np.uint8, (R, 36 * d)), (np.uint8, (R, 36 * d)), (np.uint8, (R, 36 * d)),
+            (np.int8, (R, 64 * d)), (np.int8, (R, 64 * d)), (np.uint8, (R, 64 * d)),
+            (np.float32, (R,)), (np.float32, (R,)), (np.float32, (d,)), (np.float32, (4,)),
+            (np.float16, (R, 64 * d)), (np.float16, (R, 64 * d)), (np.float16, (R, 64 * d)),
+            (np.uint8, (R, mx)), (np.uint8, (R, mx)), (np.uint8, (R, mx))]
+
+
+def ops_tag(fmt4, with16):
+    """The encoding tag prep writes into word 3 of each head's g entry."""
+    return (_lib.TAG_MARKER | (_lib.DA2_OPS_LAYOUT_VERSION << 8) | (0x10 if with16 else 0)
+            | {"nvfp4": 0, "mxfp4": 1}[fmt4])
+
+
 def sections(buf, p):
-    """Encoded operands of the ops buffer as numpy arrays [BH, R, ...]."""
-    off = api.da2_ops_offsets(p)
+    """Encoded operands of the ops buffer as numpy arrays [BH, R, ...] (the
+    sections the buffer holds for its fmt4 / with16)."""
+    off = api.da2_ops_offsets(p, buf.fmt4, buf.with16)
     raw = buf.ops.cpu().numpy()
-    BH, R, d = p.B * p.H, buf.sizes["R"], p.d
+    BH, R = p.B * p.H, buf.sizes["R"]
     out = {}
-    specs = [("Q4", np.float16, (R, 64 * d)), ("K4", np.float16, (R, 64 * d)), ("V4", np.float16, (R, 64 * d)),
-             ("Q8", np.int8, (R, 64 * d)), ("K8", np.int8, (R, 64 * d)), ("V8", np.uint8, (R, 64 * d)),
-             ("dQ", np.float32, (R,)), ("dK", np.float32, (R,)), ("dV", np.float32, (d,)), ("g", np.float32, (4,)),
-             ("Q16", np.float16, (R, 64 * d)), ("K16", np.float16, (R, 64 * d)), ("V16", np.float16, (R, 64 * d)),
-             ("Q4mx", np.uint8, (R, (d // 32 + 1) * 1024)), ("K4mx", np.uint8, (R, (d // 32 + 1) * 1024)),
-             ("V4mx", np.uint8, (R, (d // 32 + 1) * 1024))]
-    for i, (name, dt, shape) in enumerate(specs):
+    for i, (name, (dt, shape)) in enumerate(zip(SECTION_NAMES, section_specs(p, R))):
+        if off[i] < 0:
+            continue
         nbytes = BH * int(np.prod(shape)) * np.dtype(dt).itemsize
         out[name] = raw[off[i]:off[i] + nbytes].view(dt).reshape((BH,) + shape)
     return out
@@ -93,35 +111,36 @@ def expected_mx_sections(enc_mx):
             for name in ("Q", "K", "V")}
 
 
-def expected_sections(enc, enc_mx=None):
+def expected_sections(enc, enc_mx=None, fmt4="nvfp4", with16=True):
     """Oracle encodings of one head in the ops-buffer order (the MXFP4
-    sections only when ``enc_mx`` is given)."""
-    sQ = np.repeat(enc["sQ"], 16, axis=2) * enc["eQ"]
-    sK = np.repeat(enc["sK"], 16, axis=2) * enc["eK"]
-    sV = np.repeat(enc["sV"], 16, axis=1) * enc["eV"]
+    sections only when ``enc_mx`` is given; the g tag for fmt4 / with16)."""
     mx = {} if enc_mx is None else expected_mx_sections(enc_mx)
+    tag = np.array([ops_tag(fmt4, with16)], np.uint32).view(np.float32)[0]
     return {
         **mx,
-        "Q4": to_frag("Q4", sQ), "K4": to_frag("K4", sK), "V4": to_frag("V4", sV),
+        "Q4": nv_section("Q", formats.e2m1_code(enc["eQ"]), formats.e4m3_code(enc["sQ"])),
+        "K4": nv_section("K", formats.e2m1_code(enc["eK"]), formats.e4m3_code(enc["sK"])),
+        "V4": nv_section("V", formats.e2m1_code(enc["eV"]), formats.e4m3_code(enc["sV"])),
         "Q8": to_frag("Q8", enc["q8"]), "K8": to_frag("K8", enc["k8"]),
         "V8": to_frag("V8", formats.e4m3_code(enc["v8"])),
         "dQ": enc["dQ"], "dK": enc["dK"], "dV": enc["dV"],
-        "g": np.array([enc["gQ"], enc["gK"], enc["gV"], 0], np.float32),
+        "g": np.array([enc["gQ"], enc["gK"], enc["gV"], tag], np.float32),
         "Q16": to_frag("Q16", enc["q16"].astype(np.float64)), "K16": to_frag("K16", enc["k16"].astype(np.float64)),
         "V16": to_frag("V16", enc["v16"].astype(np.float64)),
     }
 
 
 def write_ops(buf, p, encs, encs_mx=None):
-    """Oracle encodings of every head -> the ops buffer (stage injection);
-    the MXFP4 sections too when ``encs_mx`` is given."""
-    off = api.da2_ops_offsets(p)
+    """Oracle encodings of every head -> the sections the ops buffer holds
+    (stage injection): the 4-bit encoding of the buffer's fmt4 (MXFP4 from
+    ``encs_mx``), the 16-bit sections when the buffer has them, and the g tag."""
+    off = api.da2_ops_offsets(p, buf.fmt4, buf.with16)
     raw = buf.ops.cpu().numpy()
-    order = ["Q4", "K4", "V4", "Q8", "K8", "V8", "dQ", "dK", "dV", "g", "Q16", "K16", "V16"]
-    if encs_mx is not None:
-        order += ["Q4mx", "K4mx", "V4mx"]
-    exp = [expected_sections(e, None if encs_mx is None else encs_mx[i]) for i, e in enumerate(encs)]
-    for i, name in enumerate(order):
+    exp = [expected_sections(e, None if encs_mx is None else encs_mx[i], buf.fmt4, buf.with16)
+           for i, e in enumerate(encs)]
+    for i, name in enumerate(SECTION_NAMES):
+        if off[i] < 0:
+            continue
         arr = np.stack([x[name] for x in exp])
         b = np.ascontiguousarray(arr).view(np.uint8).reshape(-1)
         raw[off[i]:off[i] + b.size] = b

@@ -45,7 +45,7 @@ def _run_gpu(w, Q, K, V, budgets=None, scope=None, odtype=torch.float32):
     budgets = budgets or w.budgets
     scope = scope or w.scope
     p = problem_of(w)
-    buf = api.alloc(p, scope)
+    buf = api.alloc(p, scope, fmt4=w.fmt4, with16=w.num16 > 0)
     Qd, Kd, Vd = (to_device(X, w) for X in (Q, K, V))
     O = torch.full(Qd.shape, float("nan"), dtype=odtype, device="cuda")
     api.attention(Qd, Kd, Vd, buf, w.lam, budgets, O, num16=w.num16, fmt4=w.fmt4)
@@ -128,7 +128,8 @@ def test_prep_operands(w):
     log(f"prep_operands parity {w.name}")
     Q, K, V = inputs(w)
     p = problem_of(w)
-    buf = api.alloc(p, w.scope)
+    buf = api.alloc(p, w.scope, with16=True)
+    buf.ops.fill_(0xA5)     # every section must be fully written
     Qd, Kd, Vd = (to_device(X, w) for X in (Q, K, V))
     api.da2_draft_map(Qd, Kd, buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
     api.da2_prep_operands(Qd, Kd, Vd, buf.layout, p, 1, "nvfp4", buf.stats, buf.ops, None)
@@ -138,11 +139,11 @@ def test_prep_operands(w):
     for bh in range(w.B * w.H):
         b, h = divmod(bh, w.H)
         enc = oenc.encode_head(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
-        want = expected_sections(enc)
-        for name in ("Q4", "K4", "V4", "Q16", "K16", "V16"):
+        want = expected_sections(enc, fmt4="nvfp4", with16=True)
+        for name in ("Q16", "K16", "V16"):
             gv, wv = got[name][bh].view(np.uint16), want[name].view(np.uint16)
             assert np.array_equal(gv, wv), (name, bh, int((gv != wv).sum()))
-        for name in ("Q8", "K8", "V8"):
+        for name in ("Q4", "K4", "V4", "Q8", "K8", "V8"):
             assert np.array_equal(got[name][bh], want[name]), (name, bh, int((got[name][bh] != want[name]).sum()))
         for name in ("dQ", "dK", "dV", "g"):
             assert np.array_equal(got[name][bh].view(np.uint32), want[name].view(np.uint32)), (name, bh)
@@ -155,7 +156,7 @@ def test_prep_operands_mxfp4(w):
     log(f"prep_operands mxfp4 parity {w.name}")
     Q, K, V = inputs(w)
     p = problem_of(w)
-    buf = api.alloc(p, w.scope)
+    buf = api.alloc(p, w.scope, fmt4="mxfp4")
     buf.ops.fill_(0xA5)     # the MXFP4 sections must be fully written
     Qd, Kd, Vd = (to_device(X, w) for X in (Q, K, V))
     api.da2_draft_map(Qd, Kd, buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
@@ -167,7 +168,7 @@ def test_prep_operands_mxfp4(w):
         b, h = divmod(bh, w.H)
         enc = oenc.encode_head(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
         enc_mx = oenc.encode_head_mx(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
-        want = expected_sections(enc, enc_mx)
+        want = expected_sections(enc, enc_mx, fmt4="mxfp4", with16=False)
         for name in ("Q4mx", "K4mx", "V4mx", "Q8", "K8", "V8"):
             assert np.array_equal(got[name][bh], want[name]), (name, bh, int((got[name][bh] != want[name]).sum()))
         for name in ("dQ", "dK", "dV", "g"):
@@ -196,7 +197,7 @@ def test_mixed_attn_injected(w, budgets16):
     log(f"mixed_attn stage parity {w.name} {num16} {budgets}")
     Q, K, V = inputs(w)
     p = problem_of(w)
-    buf = api.alloc(p, w.scope)
+    buf = api.alloc(p, w.scope, with16=num16 > 0)
     encs, clss, (slot2tok, n_a) = _oracle_encs_cls(w, Q, K, V, budgets, w.scope, num16)
     write_ops(buf, p, encs)
     write_lists(buf, p, clss)
@@ -232,7 +233,7 @@ def test_mixed_attn_injected_mxfp4(w, budgets16):
     log(f"mixed_attn mxfp4 stage parity {w.name} {num16} {budgets}")
     Q, K, V = inputs(w)
     p = problem_of(w)
-    buf = api.alloc(p, w.scope)
+    buf = api.alloc(p, w.scope, fmt4="mxfp4", with16=num16 > 0)
     encs, clss, (slot2tok, n_a) = _oracle_encs_cls(w, Q, K, V, budgets, w.scope, num16)
     encs_mx = [oenc.encode_head_mx(Q[b, h], K[b, h], V[b, h], slot2tok, n_a)
                for b in range(w.B) for h in range(w.H)]
@@ -493,7 +494,7 @@ def test_token_major_strided_tensors(w):
     buf_c, p, O_c = _run_gpu(w, Q, K, V)
     dev = [to_device(np.ascontiguousarray(X.transpose(0, 2, 1, 3)), w).transpose(1, 2) for X in (Q, K, V)]
     assert not dev[0].is_contiguous() and dev[0].shape == (w.B, w.H, w.N, w.d)
-    buf = api.alloc(p, w.scope)
+    buf = api.alloc(p, w.scope, fmt4=w.fmt4, with16=w.num16 > 0)
     O_store = torch.full((w.B, w.N, w.H, w.d), float("nan"), dtype=torch.float32, device="cuda")
     O = O_store.transpose(1, 2)
     api.attention(*dev, buf, w.lam, w.budgets, O, num16=w.num16, fmt4=w.fmt4)
@@ -519,7 +520,7 @@ def test_step_replays_from_a_hip_graph():
     Q, K, V = inputs(w)
     p = problem_of(w)
     dev = [to_device(X, w) for X in (Q, K, V)]
-    buf = api.alloc(p, w.scope)
+    buf = api.alloc(p, w.scope, fmt4=w.fmt4, with16=w.num16 > 0)
     O = torch.empty(dev[0].shape, dtype=torch.float32, device="cuda")
     api.attention(*dev, buf, w.lam, w.budgets, O, num16=w.num16, fmt4=w.fmt4)
     torch.cuda.synchronize()
@@ -557,3 +558,57 @@ def test_step_replays_from_a_hip_graph():
         assert all(np.array_equal(a, b) for a, b in zip(keys, ref_lists[2])), rep
         api.attention(*dev, buf, w.lam, w.budgets, O, num16=w.num16, fmt4=w.fmt4)  # eager work between replays
         torch.cuda.synchronize()
+
+
+def _meta_flags(buf, p):
+    lo = api.da2_lists_offsets(p)
+    return int(buf.lists.cpu().numpy()[lo[3] + 4:lo[3] + 8].view(np.int32)[0])
+
+
+def test_encoding_mismatch_is_flagged():
+    """The attention checks the tag that operand preparation writes: operands
+    prepared as MXFP4 but read as NVFP4, lists with 16-bit blocks but no 16-bit
+    operands, and an ops buffer nobody prepared each set their flag in the
+    lists meta word and give zero rows instead of reading sections that were
+    never written; matching calls leave the word at zero."""
+    from paper_2609_32628_amd import _lib
+    w = SMALL
+    Q, K, V = inputs(w)
+    p = problem_of(w)
+    dev = [to_device(X, w) for X in (Q, K, V)]
+    O = torch.full(dev[0].shape, float("nan"), dtype=torch.float32, device="cuda")
+
+    def run(prep_fmt4, prep16, attn_fmt4, num16, prepare=True):
+        buf = api.alloc(p, w.scope, fmt4=prep_fmt4, with16=prep16)
+        buf.ops.zero_()
+        O.fill_(float("nan"))
+        api.da2_draft_map(*dev[:2], buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
+        api.da2_rank_assign(buf.A, p, num16, *w.budgets, w.scope, buf.cls, buf.lists, buf.ws_rank)
+        if prepare:
+            api.da2_prep_operands(*dev, buf.layout, p, int(prep16), prep_fmt4, buf.stats, buf.ops, None)
+        api.da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, fmt4=attn_fmt4)
+        torch.cuda.synchronize()
+        _, counts, _ = lists_of(buf, p)
+        return _meta_flags(buf, p), O.cpu().numpy().reshape(-1, w.N, w.d), counts
+
+    flags, Og, _ = run("nvfp4", False, "nvfp4", 0)
+    assert flags == 0 and np.isfinite(Og).all() and np.abs(Og).max() > 0
+    flags, Og, _ = run("mxfp4", False, "nvfp4", 0)
+    assert flags == _lib.DA2_ATTN_ERR_FMT4 and np.all(Og == 0)
+    flags, Og, _ = run("nvfp4", False, "nvfp4", 0, prepare=False)
+    assert flags & _lib.DA2_ATTN_ERR_LAYOUT and np.all(Og == 0)
+    # 16-bit blocks in the lists, operands prepared without the 16-bit path:
+    # exactly the rows with 16-bit blocks are zero
+    flags, Og, counts = run("nvfp4", False, "nvfp4", 10)
+    assert flags == _lib.DA2_ATTN_ERR_NO16
+    slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
+    R = n_a.size
+    for bh in range(w.B * w.H):
+        for a in range(R):
+            rows = Og[bh, slot2tok[a * 64:a * 64 + n_a[a]]]
+            if counts[bh * R + a, 2] > 0:
+                assert np.all(rows == 0), (bh, a)
+            else:
+                assert np.isfinite(rows).all(), (bh, a)
+    flags, Og, _ = run("nvfp4", True, "nvfp4", 10)
+    assert flags == 0 and np.isfinite(Og).all()
