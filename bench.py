@@ -4,22 +4,25 @@ One step = the four library calls (draft_map, rank_assign, prep_operands,
 mixed_attn) over one attention layer of the mid video-DiT workload: B=1,
 12 heads, d=128, latent grid 21x30x52 = 32,760 tokens, 8x8 tiles, budgets
 10% 8-bit / 30% 4-bit / 60% skip, head-scope ranking, bf16 synthetic
-Q/K/V already resident in HBM.
+Q/K/V already resident in HBM (--workload picks another configured layer).
 
-Prints one JSON line. ``value`` is the dense-equivalent throughput of the
-whole step, 4*B*H*N^2*d flops per step; mixed_attn alone is reported too.
-The roofline object covers mixed_attn, the dominant kernel: algorithmic
-flops = retained tiles x 4*64*64*d (8-bit tiles priced at the int8/fp8
-peak, 4-bit tiles at the fp16 peak the NVFP4 path issues, or at the fp4 peak
-with --fmt4 mxfp4), divided by the
-kernel's average duration measured with HIP events on its stream. Its
-``traffic`` is the HBM bytes per launch that rocprofv3 counted for the same
-kernel source (profiles/mixed_attn_traffic.json, FETCH_SIZE and WRITE_SIZE
-scaled by a plain-copy calibration), or null when the source has changed
-since. The ``hbm`` object rates draft_map and prep_operands against HBM
-bandwidth with the bytes each call must move: draft_map reads Q and K and
-writes A; prep_operands reads Q, K and V and writes the operand sections
-that the run uses.
+Prints one JSON line. Times are medians over the timed steps, each step
+run after a 512 MiB device write that evicts the 256 MB Infinity Cache and
+timed with HIP events on the stream the calls run on; the warm (back to
+back) numbers are reported beside them. ``value`` is the dense-equivalent
+throughput of the whole step, 4*B*H*N^2*d flops per step; mixed_attn alone
+is reported too. The roofline object covers mixed_attn, the dominant
+kernel: algorithmic flops = retained tiles x 4*64*64*d, with a peak that
+weights 8-bit tiles at the int8/fp8 peak and 4-bit tiles at the fp4 peak
+(``frac``), and beside it at the peak of the MFMA the kernel issues for the
+4-bit tiles (fp16 for NVFP4, ``frac_issued_dtype``). Its ``traffic`` is the
+HBM bytes per launch that rocprofv3 counted for the same kernel source
+(profiles/mixed_attn_traffic.json, FETCH_SIZE and WRITE_SIZE scaled by a
+plain-copy calibration), or null when the source has changed since. The
+``hbm`` object rates draft_map and prep_operands against HBM bandwidth with
+the bytes each call must move: draft_map reads Q and K and writes A;
+prep_operands reads Q, K and V (V twice: the per-channel scales come first)
+and writes the operand sections the run uses.
 """
 import argparse
 import hashlib
@@ -208,46 +211,81 @@ def parse():
                     help="operator error-vs-latency sweep over sparsity, precision mixes and lambda on the "
                          "109,368-token x 56-head shape (one JSON line per point) instead of the benchmark")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-cache-study", action="store_true",
-                    help="skip the extra single mixed_attn launches (warm and with the Infinity Cache flushed); "
-                         "profiling runs use this so every profiled launch is a timed-loop launch")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 512 MiB device copy (HBM counter calibration)")
     return ap.parse_args()
 
 
-def cpu_baseline(w, Q, K, V):
-    """The oracle as it stands, on two whole heads; whole-job time extrapolated
-    linearly over heads."""
-    from threadpoolctl import threadpool_info
+def _cpu_model():
+    """Model name of the host CPU (lscpu), for the baseline record."""
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, ValueError, subprocess.SubprocessError):
+        pass
+    return "unknown"
 
+
+def _oracle_head_task(task):
+    """One oracle task (runs in a spawned worker on one BLAS thread): the
+    head-level steps (draft map, ranking, encodings) of head h, then the
+    attention of the query blocks in ``rows``. Returns the two times."""
+    from threadpoolctl import threadpool_limits
+    threadpool_limits(1)
     from oracle import attention, draft, encode, partition, rank
+    from synth import configs, gen
+    wd, h, rows = task
+    w = configs.Workload(**wd)
+    Q, K, V = gen.generate(w, heads=[h])
+    q, k, v = Q[0, 0], K[0, 0], V[0, 0]
     slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
-    R = n_a.size
-    heads = (0, 1) if w.H > 1 else (0,)
-    t_fixed = t_rows = 0.0
-    for h in heads:
-        q, k, v = Q[0, h], K[0, h], V[0, h]
-        t0 = time.perf_counter()
-        A32, _ = draft.draft_head(q, k, slot2tok, n_a, w.lam)
-        cls = rank.rank_head(A32, *w.budgets, w.scope, num16=w.num16)
-        enc = encode.encode_head(q, k, v, slot2tok, n_a)
-        ops = attention.Operands.quantized(encode.reconstruct(enc), n_a)
-        t1 = time.perf_counter()
-        for a in range(R):
-            attention.attend(ops, a, *rank.key_lists_all(cls[a]))
-        t2 = time.perf_counter()
-        t_fixed += t1 - t0
-        t_rows += t2 - t1
-    per_head = (t_fixed + t_rows) / len(heads)
-    t_job = per_head * w.H * w.B
+    t0 = time.perf_counter()
+    A32, _ = draft.draft_head(q, k, slot2tok, n_a, w.lam)
+    cls = rank.rank_head(A32, *w.budgets, w.scope, num16=w.num16)
+    enc = encode.encode_head(q, k, v, slot2tok, n_a)
+    ops = attention.Operands.quantized(encode.reconstruct(enc), n_a)
+    t1 = time.perf_counter()
+    for a in rows:
+        attention.attend(ops, a, *rank.key_lists_all(cls[a]))
+    t2 = time.perf_counter()
+    return t1 - t0, t2 - t1
+
+
+def cpu_baseline(w, rows_per_head=32):
+    """The oracle as it stands, timed on the host's cores: a process pool
+    (spawned workers, one BLAS thread each, one worker per core) runs, for
+    every head, the head-level steps (draft map, ranking, encodings) and the
+    attention of a seeded sample of query blocks. The whole job's time is
+    extrapolated to every query block of every head and divided over the
+    workers (the (head, block) tasks are independent)."""
+    from dataclasses import asdict
+    from multiprocessing import get_context
+
+    from oracle import partition
+    R = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)[1].size
+    cores = max(1, min(os.cpu_count() or 1, 64))
+    rows = sorted(int(a) for a in np.random.default_rng(13).choice(R, min(rows_per_head, R), replace=False))
+    tasks = [(asdict(w), h, rows) for h in range(w.H)]
+    t0 = time.perf_counter()
+    with get_context("spawn").Pool(min(cores, len(tasks))) as pool:
+        res = pool.map_async(_oracle_head_task, tasks, chunksize=1).get(1200)
+    wall = time.perf_counter() - t0
+    fixed = sum(r[0] for r in res)
+    per_row = sum(r[1] for r in res) / (len(res) * len(rows))
+    cpu_job = w.B * (fixed + per_row * R * w.H)       # single-core seconds for the whole job
+    t_job = cpu_job / cores
     flops = 4.0 * w.B * w.H * w.N ** 2 * w.d
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    return {"value": flops / t_job / 1e12, "unit": "TFLOP/s (dense-equivalent)", "cores": int(threads),
-            "kind": "oracle", "seconds_measured": round(t_fixed + t_rows, 2),
+    return {"value": flops / t_job / 1e12, "unit": "TFLOP/s (dense-equivalent)", "cores": cores,
+            "kind": "oracle", "cpu_model": _cpu_model(),
+            "seconds_measured_cpu": round(fixed + per_row * len(rows) * len(res), 1),
+            "seconds_measured_wall": round(wall, 1),
             "seconds_job_extrapolated": round(t_job, 1),
-            "sample": f"{len(heads)} of {w.H} heads in full (draft, ranking, encoding and the attention of all "
-                      f"{R} query blocks); whole job extrapolated linearly over heads"}
+            "sample": f"all {w.H} heads' draft map, ranking and encodings, and the attention of {len(rows)} seeded "
+                      f"query blocks per head (of {R}); process pool of {cores} single-threaded workers; the whole "
+                      f"job extrapolated to all query blocks and divided over the workers"}
 
 
 def main():
@@ -295,44 +333,45 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    # whole-step timing
+
+    def ms_of(evs):
+        return [[evs[s][i][0].elapsed_time(evs[s][i][1]) for i in range(len(stages))] for s in range(len(evs))]
+
+    # Primary: K steps, each after a 512 MiB device write that evicts the
+    # 256 MB Infinity Cache, each step and stage timed with HIP events on the
+    # stream; the median over the K steps.
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in stages] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    for s_ in range(args.steps):
+        scratch.fill_(s_ & 0xFF)
+        step(evs[s_])
+    torch.cuda.synchronize()
+    wall_flushed = time.perf_counter() - t_wall0
+    flushed = np.array(ms_of(evs))                      # [K, stages]
+    step_flushed = flushed.sum(axis=1)
+    # Beside it: K steps back to back without flushing (warm caches).
+    evw = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in stages] for _ in range(args.steps)]
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
-    for _ in range(args.steps):
-        step()
+    for s_ in range(args.steps):
+        step(evw[s_])
     e1.record(stream)
     torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / args.steps
-    # per-stage timing (events around each call)
-    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in stages] for _ in range(args.steps)]
-    for s in range(args.steps):
-        step(evs[s])
-    torch.cuda.synchronize()
-    stage_ms = {name: float(np.mean([evs[s][i][0].elapsed_time(evs[s][i][1]) for s in range(args.steps)]))
-                for i, name in enumerate(stages)}
-    # mixed_attn alone, median of single launches: back to back (warm), and
-    # after a 512 MiB write that evicts the 256 MB Infinity Cache (flushed)
-    cache_study = None
-    if not args.no_cache_study:
-        scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
-
-        def attn_median(flush, reps=10):
-            ts = []
-            for _ in range(reps):
-                if flush:
-                    scratch.fill_(1)
-                a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a0.record(stream)
-                api.da2_mixed_attn(buf.ops, buf.lists, buf.layout, p, O, fmt4=args.fmt4)
-                a1.record(stream)
-                torch.cuda.synchronize()
-                ts.append(a0.elapsed_time(a1))
-            return float(np.median(ts))
-
-        cache_study = {"mixed_attn_ms_warm_median": attn_median(False),
-                       "mixed_attn_ms_flushed_median": attn_median(True),
-                       "note": "median of 10 single launches; flushed = a 512 MiB device write before each launch"}
-        del scratch
+    ms_step_warm_mean = e0.elapsed_time(e1) / args.steps
+    warm = np.array(ms_of(evw))
+    del scratch
+    ms_step = float(np.median(step_flushed))
+    stage_ms = {name: float(np.median(flushed[:, i])) for i, name in enumerate(stages)}
+    stage_ms_warm = {name: float(np.median(warm[:, i])) for i, name in enumerate(stages)}
+    cache_study = {"step_ms_flushed_median": ms_step, "step_ms_flushed_min": float(step_flushed.min()),
+                   "step_ms_warm_median": float(np.median(warm.sum(axis=1))),
+                   "step_ms_warm_back_to_back_mean": ms_step_warm_mean,
+                   "stage_ms_warm_median": stage_ms_warm,
+                   "wall_s_flushed_loop": wall_flushed,
+                   "note": f"median over {args.steps} steps; flushed = a 512 MiB device write before each step "
+                           "(outside the events), warm = steps back to back"}
     if args.copy_calibration:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -357,8 +396,12 @@ def main():
     t_attn = stage_ms["mixed_attn"] * 1e-3
     achieved = (F8 + F4 + F16) / t_attn
     mx = args.fmt4 == "mxfp4"
-    peak4 = PEAK_FP4 if mx else PEAK_FP16
-    peak_eff = (F8 + F4 + F16) / (F8 / PEAK_8BIT + F4 / peak4 + F16 / PEAK_FP16)
+    # budget-weighted peak: 8-bit tiles at the int8/fp8 peak, 4-bit tiles at
+    # the fp4 peak (the 4-bit format's own MFMA rate), 16-bit tiles at fp16
+    peak_eff = (F8 + F4 + F16) / (F8 / PEAK_8BIT + F4 / PEAK_FP4 + F16 / PEAK_FP16)
+    # the same with 4-bit tiles at the peak of the dtype the kernel issues for
+    # them (fp16 MFMA on the exact NVFP4 values, or the scaled fp4 MFMA)
+    peak_issued = (F8 + F4 + F16) / (F8 / PEAK_8BIT + F4 / (PEAK_FP4 if mx else PEAK_FP16) + F16 / PEAK_FP16)
     dense_flops = 4.0 * w.B * w.H * w.N ** 2 * w.d
     # bytes each preparation call must move (bf16 inputs)
     sizes = buf.sizes
@@ -367,7 +410,9 @@ def main():
     # the ops buffer holds exactly the sections prep_operands writes: 8-bit
     # operands and scales, the 4-bit encoding in use, and the 16-bit operands
     # only when that path is on
-    prep_bytes = 3 * e_in + sizes["ops_bytes"]
+    # reads: Q, K, V, and V once more for the per-channel E4M3 scales, which
+    # must exist before any V block is encoded
+    prep_bytes = 4 * e_in + sizes["ops_bytes"]
     t_draft, t_prep = stage_ms["draft_map"] * 1e-3, stage_ms["prep_operands"] * 1e-3
     hbm = {"draft_map": {"bytes": draft_bytes, "GB/s": draft_bytes / t_draft / 1e9,
                          "frac": draft_bytes / t_draft / PEAK_HBM},
@@ -381,6 +426,7 @@ def main():
         "unit": "TFLOP/s (dense-equivalent, whole step)",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_note": "median over the timed steps, each with the Infinity Cache flushed first",
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": ("mixed: int8/fp8 + scaled fp4 (mxfp4) MFMA" if mx else
                   "mixed: int8/fp8 + fp16(nvfp4-exact) MFMA") + ", fp32 softmax state; bf16 in/out",
@@ -404,15 +450,19 @@ def main():
                      # recorded for the workload's own configuration only
                      "traffic": recorded_traffic(w.name) if args.partition is None and args.num16 is None
                      and not mx else None,
-                     "peak_note": "budget-weighted: 8-bit tiles at 5.0 PF (int8/fp8), 4-bit tiles at "
-                                  + ("10.1 PF (scaled fp4 MFMA, MXFP4)" if mx else
-                                     "2.5 PF (fp16 MFMA on exact NVFP4 reconstructions)")
-                                  + ", 16-bit tiles at 2.5 PF",
-                     "frac_vs_fp4_peak": achieved * (F8 / PEAK_8BIT + F4 / PEAK_FP4 + F16 / PEAK_FP16) / (F8 + F4 + F16)},
+                     "peak_note": "budget-weighted: 8-bit tiles at 5.0 PF (int8/fp8), 4-bit tiles at 10.1 PF "
+                                  "(fp4), 16-bit tiles at 2.5 PF; achieved = retained tiles x 4*64*64*d flop over "
+                                  "the flushed median of the mixed_attn launch",
+                     "frac_issued_dtype": achieved / peak_issued,
+                     "peak_issued_dtype": peak_issued / 1e12,
+                     "issued_note": "4-bit tiles at the peak of the MFMA the kernel issues for them: " +
+                                    ("10.1 PF (scaled fp4, MXFP4)" if mx else
+                                     "2.5 PF (fp16 MFMA on the exact NVFP4 values; gfx950 has no MFMA that applies "
+                                     "E4M3 scales per 16 elements)")},
         "hbm": hbm,
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(w, Q, K, V)
+        rec["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(rec), flush=True)
 
 
