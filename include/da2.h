@@ -211,7 +211,9 @@ int32_t da2_rank_assign_noalloc(const float* A, const da2_problem* p, int32_t nu
  *              [n4+n8, n4+n8+n16)
  *   [1] counts int32 [B*H*R][4] = (n4, n8, n16, 0)
  *   [2] order  int32 [B*H*R]: the work order of the rows (b*H+h)*R+a: grouped
- *              by head and by row parity, most expensive first in each group;
+ *              by head and by row parity, most expensive first in each group
+ *              (cost 3 per 4-bit or 16-bit block and 2 per 8-bit block, the
+ *              measured ratio of the attention's per-tile times);
  *              attention workgroup w takes order[(w mod 8)*ceil(n/8) + w div 8]
  *              (any permutation of the rows is a valid order)
  *   [3] meta   int32 [8]: [0] = number of rows in order; [1] = error flags

@@ -117,11 +117,11 @@ def test_rank_assign_injected(scope, budgets16):
             row = bh * R + a
             assert tuple(counts[row]) == (l4.size, l8.size, l16.size, 0)
             assert np.array_equal(keys[row, :l4.size + l8.size + l16.size], np.concatenate([l4, l8, l16]))
-    cost = 5 * counts[:, 0] + 4 * counts[:, 1] + 5 * counts[:, 2]
+    cost = 3 * counts[:, 0] + 2 * counts[:, 1] + 3 * counts[:, 2]
     group = (order // R) * 2 + (order % R) % 2          # (head, row parity) groups in ascending order
     assert np.all(np.diff(group) >= 0)
     same = np.diff(group) == 0
-    assert np.all(np.diff(cost[order])[same] <= 5 * R * 2 * BH // 8192 + 5)   # longest first within a group
+    assert np.all(np.diff(cost[order])[same] <= 3 * R * 2 * BH // 8192 + 3)   # longest first within a group
 
 
 @pytest.mark.parametrize("w", CASES + [SMALL_RAGGED, SMALL_F32], ids=lambda w: w.name)
