@@ -565,6 +565,91 @@ __device__ inline void phase_loop(const uint16_t* list, int n, const int32_t* n_
   }
 }
 
+// Double-buffered form of phase_loop for the phases whose key and value tiles
+// fit twice into sK and sV (8-bit and MXFP4 tiles at d = 64 and 128). The
+// value product of block i-1 moves into iteration i, beside the second part of
+// block i's softmax, so both halves of an iteration pair matrix work with
+// vector work, and one barrier per block suffices. Iteration i:
+//   copy K(i+2) into K buffer i%2 and V(i) into V buffer i%2
+//   region1: S' = K(i+1) Q^T interleaved with the first part of block i's softmax
+//   region2: U += V(i-1)^T P(i-1)^T interleaved with the rest of block i's softmax
+//   rescale_cur(): U *= alpha of block i
+//   wait for this wave's copies -> barrier
+// and after the last block pv_last(): U += V(n-1)^T P(n-1)^T. The accumulator
+// receives the same operations in the same order as in phase_loop (scaling by
+// alpha of block i, then the product of block i). first(S, sK0): logits of the
+// first block; region1<MASK>(Sc, Sn, Pc, nb, dk, sKn); region2<PV>(Sc, Pc, Pp,
+// sVp) with PV = false on block 0; the weights of consecutive blocks alternate
+// between two PT values, so no register copies are needed.
+template <int NFK, typename Frag, typename SA, typename PT, typename FIRST, typename STEP1, typename STEP2,
+          typename RESC, typename PVL>
+__device__ inline void phase_loop_db(const uint16_t* list, int n, const int32_t* n_a, const float* dKh,
+                                     const Frag* Kh, const Frag* Vh, Frag* sK, Frag* sV, int wave, int lane,
+                                     FIRST first_qk, STEP1 region1, STEP2 region2, RESC rescale_cur,
+                                     PVL pv_last) {
+  constexpr int TILE = NFK * 64;     // fragments per tile
+  constexpr int W0 = (NFK + 1) / 2;  // fragments wave 0 copies; wave 1 copies the rest
+  const uint32_t voff = 16u * static_cast<uint32_t>(lane);
+  const int f0 = wave ? W0 : 0, nf = wave ? NFK - W0 : W0;
+  auto dma_tile = [&](const Frag* src, Frag* dst) {
+    const char* base = reinterpret_cast<const char*>(src + f0 * 64);
+    const uint32_t lds = lds_address(dst + f0 * 64);
+    [&]<int... I>(std::integer_sequence<int, I...>) {
+      ((I < nf ? dma_fragment<(I % 4) * 1024>(base + (I / 4) * 4096, voff, lds + (I / 4) * 4096) : void()), ...);
+    }(std::make_integer_sequence<int, W0>{});
+  };
+  KeyWin win = key_window(list, 0, n, n_a, dKh, lane);
+  auto block_at = [&](int e, int first) -> int {  // e - first < 128
+    return e - first < 64 ? lane_value(win.kb, e - first) : lane_value(win.kb_next, e - first - 64);
+  };
+  // prologue: logits of block 0, then K(1) copied into the second K buffer
+  dma_tile(Kh + (int64_t)lane_value(win.kb, 0) * TILE, sK);
+  wait_vmem();
+  wg_barrier();
+  SA Sa, Sb;
+  PT Pa, Pb;
+  first_qk(Sa, sK);
+  if (n > 1) dma_tile(Kh + (int64_t)block_at(1, 0) * TILE, sK + TILE);
+  wait_vmem();
+  wait_lds();
+  wg_barrier();  // K(1) copied; both waves are done with K(0)
+
+  auto step = [&]<bool PV>(int it, SA& Sc, SA& Sn, PT& Pc, PT& Pp) {
+    const int first = it & ~63;
+    const int sl = it - first;
+    if (sl == 0 && it > 0) win = key_window(list, it, n, n_a, dKh, lane);
+    const int nb = lane_value(win.nb, sl);
+    const float dk = lane_value(win.dk, sl);
+    const int kbc = lane_value(win.kb, sl);
+    const bool more2 = it + 2 < n;
+    const int kb2 = more2 ? block_at(it + 2, first) : 0;
+    const int cur = it & 1;
+    if (more2) dma_tile(Kh + (int64_t)kb2 * TILE, sK + cur * TILE);  // K(it) was read last iteration
+    dma_tile(Vh + (int64_t)kbc * TILE, sV + cur * TILE);              // V(it-2) was read last iteration
+    // On the last block the logits of region 1 come from a stale tile and are not used.
+    if (nb < kCap)
+      region1.template operator()<true>(Sc, Sn, Pc, nb, dk, sK + (cur ^ 1) * TILE);
+    else
+      region1.template operator()<false>(Sc, Sn, Pc, nb, dk, sK + (cur ^ 1) * TILE);
+    region2.template operator()<PV>(Sc, Pc, Pp, sV + (cur ^ 1) * TILE);
+    rescale_cur();
+    wait_vmem();
+    wait_lds();
+    wg_barrier();  // K(it+2) and V(it) copied; both waves are done with K(it+1)'s other buffer and V(it-1)
+  };
+  step.template operator()<false>(0, Sa, Sb, Pa, Pb);
+  int it = 1;
+  for (; it + 1 < n; it += 2) {
+    step.template operator()<true>(it, Sb, Sa, Pb, Pa);
+    step.template operator()<true>(it + 1, Sa, Sb, Pa, Pb);
+  }
+  if (it < n) step.template operator()<true>(it, Sb, Sa, Pb, Pa);
+  if ((n - 1) & 1)
+    pv_last(Pb, sV + TILE);
+  else
+    pv_last(Pa, sV);
+}
+
 template <int D>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void mixed_attn_kernel(AttnArgs args) {
   constexpr int NS16 = D / 16, NS32 = D / 32, NT = D / 32;
@@ -744,13 +829,14 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
       Qf[s] = Qa[(qt * NS64 + s) * 64 + lane];
       qsc[s] = qt ? qsw[NS64 + s] : qsw[s];
     }
-    i32x4* sKm = reinterpret_cast<i32x4*>(sK);
-    i32x4* sVm = reinterpret_cast<i32x4*>(sV);
-    i32x4 P;
-    int psc = 0;
     float alpha = 1.0f;
     typedef f32x16 SA[2];
-    auto qk = [&](SA& S) {
+    struct PT {
+      i32x4 P;  // E2M1 weight codes of the block's two 16-slot groups per lane
+      int psc;  // their E8M0 scale word
+    };
+    auto qk = [&](SA& S, const f16x8* sK0) {
+      const i32x4* sKm = reinterpret_cast<const i32x4*>(sK0);
       const i32x4 ksw = sKm[2 * NS64 * 64 + lane];
       S[0] = S[1] = f32x16{};
 #pragma unroll
@@ -763,8 +849,9 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
     float off = 0.0f, sum = 0.0f;
     int ke = 0;
     // Region 1: logits of the next block (NS64 stages of two MFMAs) with the
-    // maxima, the block exponent and the first half of the weights.
-    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float) {
+    // maxima, the block exponent and the first quarter of the weights.
+    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, PT& Pc, int nb, float, const f16x8* sKn) {
+      const i32x4* sKm = reinterpret_cast<const i32x4*>(sKn);
       if constexpr (MASK) mask_tail_mx(Sc, nb, g);
       const i32x4 ksw = sKm[2 * NS64 * 64 + lane];
       i32x4 k0 = sKm[lane], k1 = sKm[NS64 * 64 + lane];
@@ -788,8 +875,7 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
             off = -mn - (float)ke;
           } else {
             sum = 0.0f;
-            P[0] = mx_codes8<0>(Sc[0], c4, off, sum);
-            P[1] = mx_codes8<8>(Sc[0], c4, off, sum);
+            Pc.P[0] = mx_codes8<0>(Sc[0], c4, off, sum);
           }
         }
         fence();
@@ -797,24 +883,40 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
         k1 = n1;
       }
     };
-    // Region 2: the second half of the weights, the scale word and l.
-    auto region2 = [&](SA& Sc) {
-      P[2] = mx_codes8<0>(Sc[1], c4, off, sum);
-      P[3] = mx_codes8<8>(Sc[1], c4, off, sum);
-      psc = ke + 127;
-      l += __builtin_amdgcn_ldexpf(sum, ke);  // Pt = 2^k y, exact scaling
-      after(P), after(l), after(psc);
-    };
-    // U += V^T P^T: one scaled MFMA per channel tile.
-    auto pv = [&](SA& Sc) {
-      if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+    // Region 2: U += V^T P^T of the previous block (one scaled MFMA per
+    // channel tile) beside the rest of the weights, the scale word and l.
+    auto region2 = [&]<bool PV>(SA& Sc, PT& Pc, PT& Pp, const f16x8* sVp) {
+      const i32x4* sVm = reinterpret_cast<const i32x4*>(sVp);
       const i32x4 vsw = sVm[NT * 64 + lane];
 #pragma unroll
-      for (int t = 0; t < NT; ++t) U[t] = mfma_fp4(sVm[t * 64 + lane], P, U[t], vsw[t], psc);
+      for (int t = 0; t < NT; ++t) {
+        if constexpr (PV) U[t] = mfma_fp4(sVm[t * 64 + lane], Pp.P, U[t], vsw[t], Pp.psc);
+        // the three remaining groups of eight weights over the NT products
+#pragma unroll
+        for (int q = 1; q < 4; ++q) {
+          if ((q - 1) * NT / 3 != t) continue;
+          if (q == 1) Pc.P[1] = mx_codes8<8>(Sc[0], c4, off, sum);
+          if (q == 2) Pc.P[2] = mx_codes8<0>(Sc[1], c4, off, sum);
+          if (q == 3) Pc.P[3] = mx_codes8<8>(Sc[1], c4, off, sum);
+        }
+        fence();
+      }
+      Pc.psc = ke + 127;
+      l += __builtin_amdgcn_ldexpf(sum, ke);  // Pt = 2^k y, exact scaling
     };
-    phase_loop<NFM, i32x4, SA>(keys, n4, L.n_a, dKh, reinterpret_cast<const i32x4*>(args.K4mx) + blk0 * (NFM * 64),
-                               reinterpret_cast<const i32x4*>(args.V4mx) + blk0 * (NFM * 64), sKm, sVm, wave, lane,
-                               qk, region1, region2, pv);
+    auto rescale_cur = [&]() {
+      if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+    };
+    auto pv_last = [&](PT& Pp, const f16x8* sVp) {
+      const i32x4* sVm = reinterpret_cast<const i32x4*>(sVp);
+      const i32x4 vsw = sVm[NT * 64 + lane];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) U[t] = mfma_fp4(sVm[t * 64 + lane], Pp.P, U[t], vsw[t], Pp.psc);
+    };
+    static_assert(2 * NFM * 1024 <= sizeof(sK) && 2 * NFM * 1024 <= sizeof(sV), "two MXFP4 tiles fit");
+    phase_loop_db<NFM, f16x8, SA, PT>(keys, n4, L.n_a, dKh, reinterpret_cast<const f16x8*>(args.K4mx) + blk0 * (NFM * 64),
+                                      reinterpret_cast<const f16x8*>(args.V4mx) + blk0 * (NFM * 64), sK, sV, wave,
+                                      lane, qk, region1, region2, rescale_cur, pv_last);
   }
 
   // per-lane channel of accumulator register i of channel tile t
@@ -840,12 +942,10 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
 #pragma unroll
     for (int s = 0; s < NS32; ++s) Qf[s] = Qa[(qt * NS32 + s) * 64 + lane];
     const float c8a = args.dQ[blk0 + a] * kLog2e * rsqd;
-    i32x4* sK8 = reinterpret_cast<i32x4*>(sK);
-    i32x4* sV8 = reinterpret_cast<i32x4*>(sV);
-    i32x8 P;
     float alpha = 1.0f;
     typedef i32x16 SA[2];
-    auto qk = [&](SA& S) {
+    auto qk = [&](SA& S, const f16x8* sK0) {
+      const i32x4* sK8 = reinterpret_cast<const i32x4*>(sK0);
       S[0] = S[1] = i32x16{};
 #pragma unroll
       for (int s = 0; s < NS32; ++s)
@@ -855,11 +955,12 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
     };
     // Softmax state of the current block, shared by the two regions.
     f32x16 sf[2];
-    float cb = 0.0f, off = 0.0f, s0 = 0.0f, s1 = 0.0f;
-    int w[8];
+    float cb = 0.0f, off = 0.0f, s0 = 0.0f;
+    int w[2];
     // Region 1: logits of the next block (NS32 stages of two int8 MFMAs) with
-    // the conversion, the row maxima and the first half of the weights.
-    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, int nb, float dk) {
+    // the conversion, the row maxima and the first quarter of the weights.
+    auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, i32x8&, int nb, float dk, const f16x8* sKn) {
+      const i32x4* sK8 = reinterpret_cast<const i32x4*>(sKn);
       cb = c8a * dk;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
@@ -880,48 +981,64 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
 #pragma unroll
         for (int piece = 0; piece < NP; ++piece) {
           if (piece * NS32 / NP != s) continue;
-          if (piece == 0) {
+          if (piece == 0)
             off = kExpOffset - new_max(fmaxf(max16(sf[0]), max16(sf[1])), cb, m, l, alpha);
-          } else {
+          else
             s0 = fp8_weights8<0>(sf[0], cb, off, w[0], w[1]);
-            s1 = fp8_weights8<8>(sf[0], cb, off, w[2], w[3]);
-          }
         }
         fence();
         k0 = n0;
         k1 = n1;
       }
     };
-    // Region 2: the second half of the weights and the fp8 P^T operand.
-    auto region2 = [&](SA&) {
-      const float s2 = fp8_weights8<0>(sf[1], cb, off, w[4], w[5]);
-      const float s3 = fp8_weights8<8>(sf[1], cb, off, w[6], w[7]);
-      P = i32x8{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]};
-      l += (s0 + s1) + (s2 + s3);
-      after(P), after(l);
+    // Region 2: U += V^T P^T of the previous block (fp8 x fp8, unit scales;
+    // value fragments read one MFMA ahead) beside the remaining three quarters
+    // of the weights, the fp8 P^T operand and l.
+    auto vfrag = [&](const i32x4* sV8, int t) {
+      const i32x4 v0 = sV8[(t * 2 + 0) * 64 + lane], v1 = sV8[(t * 2 + 1) * 64 + lane];
+      return i32x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
     };
-    // U += V^T P^T (fp8 x fp8, unit scales); value fragments read one MFMA ahead.
-    auto pv = [&](SA& Sc) {
-      if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
-      auto vfrag = [&](int t) {
-        const i32x4 v0 = sV8[(t * 2 + 0) * 64 + lane], v1 = sV8[(t * 2 + 1) * 64 + lane];
-        return i32x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-      };
-      i32x8 vf = vfrag(0);
+    auto region2 = [&]<bool PV>(SA&, i32x8& Pc, i32x8& Pp, const f16x8* sVp) {
+      const i32x4* sV8 = reinterpret_cast<const i32x4*>(sVp);
+      float s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+      int w2[6];
+      i32x8 vf;
+      if constexpr (PV) vf = vfrag(sV8, 0);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const i32x8 cur = vf;
-        if (t + 1 < NT) vf = vfrag(t + 1);
-        U[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur, P, U[t], 0, 0, 0, 127, 0, 127);
+        if constexpr (PV) {
+          const i32x8 cur = vf;
+          if (t + 1 < NT) vf = vfrag(sV8, t + 1);
+          U[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur, Pp, U[t], 0, 0, 0, 127, 0, 127);
+        }
+#pragma unroll
+        for (int q = 1; q < 4; ++q) {
+          if ((q - 1) * NT / 3 != t) continue;
+          if (q == 1) s1 = fp8_weights8<8>(sf[0], cb, off, w2[0], w2[1]);
+          if (q == 2) s2 = fp8_weights8<0>(sf[1], cb, off, w2[2], w2[3]);
+          if (q == 3) s3 = fp8_weights8<8>(sf[1], cb, off, w2[4], w2[5]);
+        }
         fence();
       }
+      Pc = i32x8{w[0], w[1], w2[0], w2[1], w2[2], w2[3], w2[4], w2[5]};
+      l += (s0 + s1) + (s2 + s3);
+    };
+    auto rescale_cur = [&]() {
+      if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
+    };
+    auto pv_last = [&](i32x8& Pp, const f16x8* sVp) {
+      const i32x4* sV8 = reinterpret_cast<const i32x4*>(sVp);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        U[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vfrag(sV8, t), Pp, U[t], 0, 0, 0, 127, 0, 127);
     };
     wait_lds();
     wg_barrier();  // the NVFP4 phase is done with sK / sV
-    phase_loop<2 * NS32, i32x4, SA>(keys + n4, n8, L.n_a, dKh,
-                                 reinterpret_cast<const i32x4*>(args.K8) + blk0 * (kCap * D / 16),
-                                 reinterpret_cast<const i32x4*>(args.V8) + blk0 * (kCap * D / 16), sK8, sV8, wave,
-                                 lane, qk, region1, region2, pv);
+    static_assert(2 * 2 * NS32 * 1024 <= sizeof(sK) && 2 * 2 * NS32 * 1024 <= sizeof(sV), "two 8-bit tiles fit");
+    phase_loop_db<2 * NS32, f16x8, SA, i32x8>(keys + n4, n8, L.n_a, dKh,
+                                             reinterpret_cast<const f16x8*>(args.K8) + blk0 * (kCap * D / 16),
+                                             reinterpret_cast<const f16x8*>(args.V8) + blk0 * (kCap * D / 16), sK, sV,
+                                             wave, lane, qk, region1, region2, rescale_cur, pv_last);
     // Exit: U_c <- eta delta_c U_c, l <- eta l
 #pragma unroll
     for (int t = 0; t < NT; ++t)
