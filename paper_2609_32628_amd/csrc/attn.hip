@@ -895,14 +895,17 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
 #pragma unroll
         for (int q = 1; q < 4; ++q) {
           if ((q - 1) * NT / 3 != t) continue;
-          if (q == 1) Pc.P[1] = mx_codes8<8>(Sc[0], c4, off, sum);
-          if (q == 2) Pc.P[2] = mx_codes8<0>(Sc[1], c4, off, sum);
-          if (q == 3) Pc.P[3] = mx_codes8<8>(Sc[1], c4, off, sum);
+          // each piece's results are used in its stage, which keeps the piece there
+          if (q == 1) Pc.P[1] = mx_codes8<8>(Sc[0], c4, off, sum), after(Pc.P[1]), after(sum);
+          if (q == 2) Pc.P[2] = mx_codes8<0>(Sc[1], c4, off, sum), after(Pc.P[2]), after(sum);
+          if (q == 3) Pc.P[3] = mx_codes8<8>(Sc[1], c4, off, sum), after(Pc.P[3]), after(sum);
         }
         fence();
       }
       Pc.psc = ke + 127;
       l += __builtin_amdgcn_ldexpf(sum, ke);  // Pt = 2^k y, exact scaling
+      // computed here, beside the products (not sunk into the next iteration)
+      after(Pc.P), after(Pc.psc), after(l);
     };
     auto rescale_cur = [&]() {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
@@ -961,13 +964,13 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
     // the conversion, the row maxima and the first quarter of the weights.
     auto region1 = [&]<bool MASK>(SA& Sc, SA& Sn, i32x8&, int nb, float dk, const f16x8* sKn) {
       const i32x4* sK8 = reinterpret_cast<const i32x4*>(sKn);
+      i32x4 k0 = sK8[lane], k1 = sK8[NS32 * 64 + lane];
       cb = c8a * dk;
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int i = 0; i < 16; ++i) sf[j][i] = (float)Sc[j][i];
       if constexpr (MASK) mask_tail(sf, nb, g);
-      i32x4 k0 = sK8[lane], k1 = sK8[NS32 * 64 + lane];
       constexpr int NP = 2;
 #pragma unroll
       for (int s = 0; s < NS32; ++s) {
@@ -1014,14 +1017,17 @@ __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2))) void m
 #pragma unroll
         for (int q = 1; q < 4; ++q) {
           if ((q - 1) * NT / 3 != t) continue;
-          if (q == 1) s1 = fp8_weights8<8>(sf[0], cb, off, w2[0], w2[1]);
-          if (q == 2) s2 = fp8_weights8<0>(sf[1], cb, off, w2[2], w2[3]);
-          if (q == 3) s3 = fp8_weights8<8>(sf[1], cb, off, w2[4], w2[5]);
+          // each piece's results are used in its stage, which keeps the piece there
+          if (q == 1) s1 = fp8_weights8<8>(sf[0], cb, off, w2[0], w2[1]), after(s1), after(w2[0]), after(w2[1]);
+          if (q == 2) s2 = fp8_weights8<0>(sf[1], cb, off, w2[2], w2[3]), after(s2), after(w2[2]), after(w2[3]);
+          if (q == 3) s3 = fp8_weights8<8>(sf[1], cb, off, w2[4], w2[5]), after(s3), after(w2[4]), after(w2[5]);
         }
         fence();
       }
       Pc = i32x8{w[0], w[1], w2[0], w2[1], w2[2], w2[3], w2[4], w2[5]};
       l += (s0 + s1) + (s2 + s3);
+      // computed here, beside the products (not sunk into the next iteration)
+      after(Pc), after(l);
     };
     auto rescale_cur = [&]() {
       if (__ballot(alpha != 1.0f)) rescale<NT>(U, alpha);
