@@ -83,6 +83,35 @@ def test_draft_map(w):
         assert stats[bh, 1] == np.float32(np.abs(K[b, h]).max()).view(np.uint32)
 
 
+# Draft map at full row lengths: several 128x128 logit tiles with ragged last
+# tiles, and both register forms of the row softmax (up to 10 entries per lane
+# for rows of up to 640 blocks, up to 32 beyond).
+DRAFT_SIZES = [replace(configs.MID, name="draft-6x30x52-h2", T=6, H=2),      # R = 168
+               replace(configs.MID, name="draft-21x30x52-h2", H=2),          # R = 588
+               replace(configs.WIDE, name="draft-21x45x80-h2", H=2)]         # R = 1260
+
+
+@pytest.mark.parametrize("w", DRAFT_SIZES, ids=lambda w: w.name)
+def test_draft_map_row_lengths(w):
+    log(f"draft_map parity {w.name}")
+    Q, K, V = inputs(w)
+    p = problem_of(w)
+    buf = api.alloc(p, w.scope)
+    api.da2_draft_map(to_device(Q, w), to_device(K, w), buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
+    torch.cuda.synchronize()
+    slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
+    R = n_a.size
+    A = buf.A.cpu().numpy().reshape(-1, R, R)
+    stats = buf.stats.cpu().numpy().view(np.uint32).reshape(A.shape[0], 4 + w.d)
+    for bh in range(A.shape[0]):
+        A32, _ = odraft.draft_head(Q[0, bh], K[0, bh], slot2tok, n_a, w.lam)
+        rel = np.abs(A[bh].astype(np.float64) - A32) / np.maximum(A32, 1e-30)
+        log(f"  R={R} head {bh}: A max rel diff {rel.max():.2e}, differing entries {(A[bh] != A32).sum()}")
+        assert rel.max() <= 1e-6
+        assert stats[bh, 0] == np.float32(np.abs(Q[0, bh]).max()).view(np.uint32)
+        assert stats[bh, 1] == np.float32(np.abs(K[0, bh]).max()).view(np.uint32)
+
+
 def _tie_heavy(R, seed):
     rng = np.random.default_rng(seed)
     A = rng.random((R, R)).astype(np.float32)
