@@ -448,6 +448,9 @@ def main():
         "exp_floor_ms": exp_floor_ms,
         "cache_study": cache_study,
         "roofline": {"bound": "mfma", "kernel": "mixed_attn_kernel", "achieved": achieved / 1e12,
+                     "limiter": "vector ALU: the softmax of every phase and, for NVFP4, the decode of the packed "
+                                "K/V tiles issue more VALU cycles than the tiles' MFMAs (per-phase counters in "
+                                "profiles/mixed_attn_phases_mid-21x30x52-h12-d128.md)",
                      "peak": peak_eff / 1e12, "unit": "TFLOP/s", "frac": achieved / peak_eff,
                      # recorded for the workload's own configuration only
                      "traffic": recorded_traffic(w.name) if args.partition is None and args.num16 is None
