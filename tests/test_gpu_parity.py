@@ -461,6 +461,14 @@ def test_budget_sweep(w):
     _full_size(w, out_heads=(5, 10), n_rows=24, seed=3)
 
 
+@pytest.mark.parametrize("fmt4", ["nvfp4", "mxfp4"])
+def test_all_pairs_4bit(fmt4):
+    """Every pair on the 4-bit path (no skip): rows of all 588 key blocks in
+    one phase, so the key window is refilled nine times per row."""
+    w = replace(configs.MID, name=f"mid-all4bit-{fmt4}", budgets=(0, 100, 100), fmt4=fmt4)
+    _full_size(w, out_heads=(7,), n_rows=8, seed=13)
+
+
 def test_wide_layer():
     """Wide layer: 40 heads, 21x45x80 = 75,600 tokens, 1% key outliers x8:
     every head's class map, outputs of two heads on sampled blocks."""
