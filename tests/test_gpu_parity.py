@@ -469,6 +469,15 @@ def test_all_pairs_4bit(fmt4):
     _full_size(w, out_heads=(7,), n_rows=8, seed=13)
 
 
+@pytest.mark.parametrize("w", [replace(configs.MID, name="mid-row-scope", scope="row"),
+                               replace(configs.LONG, name="long-row-scope", scope="row")], ids=lambda w: w.name)
+def test_row_scope_full_size(w):
+    """Row-scope ranking at full size: each query block's R key blocks sorted
+    in LDS (R = 588 and R = 1,980, sorted as 1,024 and 2,048 keys); every
+    class map, sampled output rows of one head."""
+    _full_size(w, out_heads=(1,), n_rows=8, seed=14)
+
+
 def test_wide_layer():
     """Wide layer: 40 heads, 21x45x80 = 75,600 tokens, 1% key outliers x8:
     every head's class map, outputs of two heads on sampled blocks."""
