@@ -88,7 +88,9 @@ def test_draft_map(w):
 # for rows of up to 640 blocks, up to 32 beyond).
 DRAFT_SIZES = [replace(configs.MID, name="draft-6x30x52-h2", T=6, H=2),      # R = 168
                replace(configs.MID, name="draft-21x30x52-h2", H=2),          # R = 588
-               replace(configs.WIDE, name="draft-21x45x80-h2", H=2)]         # R = 1260
+               replace(configs.WIDE, name="draft-21x45x80-h2", H=2),         # R = 1260
+               replace(configs.MID, name="draft-21x30x52-h2-lam0", H=2, lam=0.0),  # average pooling alone
+               replace(configs.MID, name="draft-21x30x52-h2-lam1", H=2, lam=1.0)]  # max pooling alone
 
 
 @pytest.mark.parametrize("w", DRAFT_SIZES, ids=lambda w: w.name)
