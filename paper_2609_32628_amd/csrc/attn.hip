@@ -437,14 +437,19 @@ __device__ inline void nv_phase_loop(const uint16_t* list, int n, const int32_t*
   wg_barrier();
   SA Sa, Sb;
   first_qk(Sa);
-  if (n > 1) nv_load_qk<D>(kx, Kh + (int64_t)block_at(1, 0) * NB, wave, lane);
+  // The packed loads here and in the loop are issued on every path (past the
+  // end of the list they fetch block 0, which is never decoded into a tile
+  // that is read): where paths with different numbers of loads in flight
+  // join, the compiler waits for all of them, including the share that the
+  // next region does not need yet.
+  nv_load_qk<D>(kx, Kh + (int64_t)(n > 1 ? block_at(1, 0) : 0) * NB, wave, lane);
   wait_lds();
   wg_barrier();  // both waves have read K(0)
   if (n > 1) {
 #pragma unroll
     for (int f = 0; f < NS16; ++f) kdec(f);
   }
-  if (n > 2) nv_load_qk<D>(kx, Kh + (int64_t)block_at(2, 0) * NB, wave, lane);
+  nv_load_qk<D>(kx, Kh + (int64_t)(n > 2 ? block_at(2, 0) : 0) * NB, wave, lane);
   wait_lds();
   wg_barrier();  // K(1) is in sK
 
@@ -461,14 +466,14 @@ __device__ inline void nv_phase_loop(const uint16_t* list, int n, const int32_t*
       region1.template operator()<true>(Sc, Sn, nb, vdec);
     else
       region1.template operator()<false>(Sc, Sn, nb, vdec);
-    if (more1) nv_load_v<D>(vx, Vh + (int64_t)kb1 * NB, wave, lane);
+    nv_load_v<D>(vx, Vh + (int64_t)kb1 * NB, wave, lane);
     wait_lds();
     wg_barrier();  // sV holds V(it); both waves are done with sK
     // K(it+2) is decoded unconditionally: past the end of the list the share
     // holds the previous block and the tile it writes is never read (one
     // instantiation of pv keeps the register allocation of the loop small)
     pv(Sc, kdec);
-    if (more3) nv_load_qk<D>(kx, Kh + (int64_t)kb3 * NB, wave, lane);
+    nv_load_qk<D>(kx, Kh + (int64_t)kb3 * NB, wave, lane);
     wait_lds();
     wg_barrier();  // sK holds K(it+2); both waves are done with sV
   };
