@@ -100,61 +100,73 @@ __global__ __launch_bounds__(256) void draft_pool_kernel(DraftArgs args) {
 
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-// One 128x128 logit tile of one branch (blockIdx.z = 2*head + branch) on the
-// float64 matrix cores: each wave owns a 64x64 quarter as 4x4 MFMA tiles of
-// 16x16x4, so every operand value loaded feeds four MFMAs. The reduction over
-// channels may visit them in any order as long as both operands agree: lane
-// group q = lane/16 of k-step 2t+h reads channel 8t + 2q + h, so one 16-byte
-// load per operand tile feeds two k-steps. The loads run one group of 8
-// channels ahead of the MFMAs, and consecutive MFMAs update different
-// accumulators. Rows and columns beyond R read row R-1 and are not stored.
-constexpr int kLogitTile = 128;
+// One 128x160 logit tile of one branch (blockIdx.z = 2*head + branch) on the
+// float64 matrix cores: each wave owns a 64x80 quarter as 4x5 MFMA tiles of
+// 16x16x4, so every query value loaded feeds five MFMAs and every key value
+// four. (On R = 588 this makes 1,920 waves, which two waves per SIMD take in
+// one round; 64x64 quarters made 2,400 and a thin second round.) The
+// reduction over channels may visit them in any order as long as both
+// operands agree: lane group q = lane/16 of k-step 2t+h reads channel
+// 8t + 2q + h, so one 16-byte load per operand tile feeds two k-steps. The
+// loads run one group of 8 channels ahead of the MFMAs, and consecutive MFMAs
+// update different accumulators. Operand rows are addressed as 32-bit byte
+// offsets from the branch's base (one VGPR each), which keeps the kernel
+// within 256 VGPRs. Rows and columns beyond R read row R-1 and are not stored.
+constexpr int kLogitTile = 128;  // rows per workgroup
+constexpr int kLogitCols = 160;  // columns per workgroup
 template <int D>
 __global__ __launch_bounds__(256) void draft_logits_kernel(DraftArgs args) {
-  constexpr int d = D, NI = 4;
+  constexpr int d = D, NI = 4, NJ = 5;
   const int R = args.R, bh = blockIdx.z >> 1, br = blockIdx.z & 1;
   const double* Qs = (br == 0 ? args.Qbar : args.Qmax) + (int64_t)bh * R * d;
   const double* Ks = (br == 0 ? args.Kbar : args.Kmax) + (int64_t)bh * R * d;
   double* out = (br == 0 ? args.S1 : args.S2) + (int64_t)bh * R * R;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, li = lane & 15, q = lane >> 4;
-  const int r0 = blockIdx.y * kLogitTile + (wave >> 1) * 64, c0 = blockIdx.x * kLogitTile + (wave & 1) * 64;
-  const double* pa[NI];
-  const double* pb[NI];
+  const int r0 = blockIdx.y * kLogitTile + (wave >> 1) * 64, c0 = blockIdx.x * kLogitCols + (wave & 1) * 80;
+  // byte offsets of each lane's operand rows from the branch's base (one VGPR each)
+  uint32_t oa[NI], ob[NJ];
 #pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    pa[i] = Qs + (int64_t)min(r0 + 16 * i + li, R - 1) * d + 2 * q;
-    pb[i] = Ks + (int64_t)min(c0 + 16 * i + li, R - 1) * d + 2 * q;
-  }
-  f64x4 acc[NI][NI];
+  for (int i = 0; i < NI; ++i) oa[i] = (uint32_t)(min(r0 + 16 * i + li, R - 1) * d + 2 * q) * 8u;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) ob[j] = (uint32_t)(min(c0 + 16 * j + li, R - 1) * d + 2 * q) * 8u;
+  auto lda = [&](int i, int t) {
+    return *reinterpret_cast<const double2*>(reinterpret_cast<const char*>(Qs) + oa[i] + 64 * t);
+  };
+  auto ldb = [&](int j, int t) {
+    return *reinterpret_cast<const double2*>(reinterpret_cast<const char*>(Ks) + ob[j] + 64 * t);
+  };
+  f64x4 acc[NI][NJ];
 #pragma unroll
   for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int j = 0; j < NI; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
-  double2 a[2][NI], b[2][NI];  // [buffer][tile]
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+  double2 a[2][NI], b[2][NJ];  // [buffer][tile]
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
-    a[0][i] = *reinterpret_cast<const double2*>(pa[i]);
-    b[0][i] = *reinterpret_cast<const double2*>(pb[i]);
+    a[0][i] = lda(i, 0);
   }
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) b[0][j] = ldb(j, 0);
 #pragma unroll
   for (int t = 0; t < d / 8; ++t) {
     const int cur = t & 1;
     if (t + 1 < d / 8) {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        a[cur ^ 1][i] = *reinterpret_cast<const double2*>(pa[i] + 8 * (t + 1));
-        b[cur ^ 1][i] = *reinterpret_cast<const double2*>(pb[i] + 8 * (t + 1));
+        a[cur ^ 1][i] = lda(i, t + 1);
       }
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) b[cur ^ 1][j] = ldb(j, t + 1);
     }
 #pragma unroll
     for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < NI; ++j)
+      for (int j = 0; j < NJ; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[cur][i].x, b[cur][j].x, acc[i][j], 0, 0, 0);
 #pragma unroll
     for (int i = 0; i < NI; ++i)
 #pragma unroll
-      for (int j = 0; j < NI; ++j)
+      for (int j = 0; j < NJ; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[cur][i].y, b[cur][j].y, acc[i][j], 0, 0, 0);
   }
   // workgroup (0, 0, 2 head + branch) also reduces the per-block max |Q|
@@ -176,7 +188,7 @@ __global__ __launch_bounds__(256) void draft_logits_kernel(DraftArgs args) {
 #pragma unroll
   for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int j = 0; j < NI; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int row = r0 + 16 * i + q + 4 * e, col = c0 + 16 * j + li;
@@ -275,11 +287,11 @@ hipError_t launch_draft(const DraftArgs& args, hipStream_t stream) {
     else
       hipLaunchKernelGGL((draft_pool_kernel<64, float>), pool_grid, dim3(256), 0, stream, args);
   }
-  const int nt = (args.R + kLogitTile - 1) / kLogitTile;
+  const int nt = (args.R + kLogitTile - 1) / kLogitTile, ntc = (args.R + kLogitCols - 1) / kLogitCols;
   if (args.d == 128)
-    hipLaunchKernelGGL(draft_logits_kernel<128>, dim3(nt, nt, 2 * BH), dim3(256), 0, stream, args);
+    hipLaunchKernelGGL(draft_logits_kernel<128>, dim3(ntc, nt, 2 * BH), dim3(256), 0, stream, args);
   else
-    hipLaunchKernelGGL(draft_logits_kernel<64>, dim3(nt, nt, 2 * BH), dim3(256), 0, stream, args);
+    hipLaunchKernelGGL(draft_logits_kernel<64>, dim3(ntc, nt, 2 * BH), dim3(256), 0, stream, args);
   const int64_t rows = (int64_t)BH * args.R;
   const dim3 sgrid((unsigned)((rows + 3) / 4));
   if (args.R <= 64 * 10)
