@@ -13,9 +13,11 @@
 // kernel spread over many workgroups, then a one-workgroup scan per head that
 // fixes the next digit. The third pass also collects the keys that match a
 // cut's 22-bit prefix (the threshold is one of them); when there are at most
-// kRankCand of them, its scan sorts them and reads the threshold key directly,
-// and the last two passes skip that cut. Row scope sorts each row's R keys in
-// LDS (bitonic).
+// kRankCand of them, its scan sorts them and reads the threshold key directly.
+// A cut with more (ties, or a dense bin) takes the last two passes inside that
+// scan's workgroup, over the head's scores with an LDS histogram, so the host
+// launches three histogram passes in every case. Row scope sorts each row's R
+// keys in LDS (bitonic).
 #include <mutex>
 
 #include "common.hpp"
@@ -177,22 +179,79 @@ __device__ inline uint32_t block_exscan_256(uint32_t v, uint32_t* sh, uint32_t* 
   return base + x - v;
 }
 
+// Fixes the next digit of cut t from a histogram h of the digit (2048 bins,
+// global or LDS) in which the cut's keys are counted: thread i owns bins
+// [2047-8i-7, 2047-8i], visited from the top, and the thread whose run holds
+// rank k appends the digit to the cut's prefix and keeps the rank left inside
+// that bin. Called by all 256 threads; returns after a barrier.
+__device__ inline void scan_digit(const uint32_t* h, int s, int64_t k, uint64_t& prefix, int64_t& kleft,
+                                  uint32_t* sh) {
+  uint32_t c[8], local = 0;
+  for (int q = 0; q < 8; ++q) {
+    c[q] = h[kBins - 1 - 8 * threadIdx.x - q];
+    local += c[q];
+  }
+  uint32_t total;
+  const uint32_t before = block_exscan_256(local, sh, &total);
+  if ((int64_t)before < k && k <= (int64_t)before + local) {
+    uint32_t run = before;
+    for (int q = 0; q < 8; ++q) {
+      if (k <= (int64_t)run + c[q]) {
+        const uint64_t dig = kBins - 1 - 8 * threadIdx.x - q;
+        prefix |= dig << s;
+        kleft = k - run;
+        break;
+      }
+      run += c[q];
+    }
+  }
+  __syncthreads();
+}
+
+// Histogram slots of the pass whose digit ends at bit hi, from the cuts'
+// prefixes and ranks left (the same rule as hist_slots).
+__device__ inline void slots_of(const uint64_t* prefix, const int64_t* kleft, int hi, int (&slot)[kCuts],
+                                uint64_t (&pre)[kCuts]) {
+  for (int t = 0; t < kCuts; ++t) {
+    pre[t] = prefix[t] >> hi;
+    slot[t] = kleft[t] > 0 ? t : -1;
+    for (int u = 0; u < t && slot[t] == t; ++u)
+      if (slot[u] == u && pre[u] == pre[t]) slot[t] = u;
+  }
+}
+
+// One workgroup per head: fixes this pass's digit of every cut from the
+// global histogram. The cuts' prefixes and ranks left are held in LDS while
+// the workgroup works and written back at the end. The collecting pass first
+// resolves each cut whose candidate list is complete by sorting it; a cut still
+// open after that (its 22-bit prefix is shared by more keys than the list
+// holds: ties or a dense bin) takes the remaining passes here, over the head's
+// scores with an LDS histogram, so the host launches no further passes.
 __global__ __launch_bounds__(256) void rank_scan_kernel(RankArgs args, int pass) {
   __shared__ uint32_t sh[4];
-  __shared__ uint64_t sk[kRankCand];
+  // candidate keys; in the remaining passes, the cuts' digit histograms
+  constexpr int kSkWords = kRankCand > kCuts * kBins / 2 ? kRankCand : kCuts * kBins / 2;
+  __shared__ uint64_t sk[kSkWords];
+  __shared__ uint64_t s_prefix[kCuts];
+  __shared__ int64_t s_kleft[kCuts];
   const int bh = blockIdx.x;
   const int s = kShift[pass];
   uint32_t* gh = args.hist + (int64_t)bh * kCuts * kBins;
+  if (threadIdx.x < kCuts) {
+    s_prefix[threadIdx.x] = args.prefix[bh * kCuts + threadIdx.x];
+    s_kleft[threadIdx.x] = args.kleft[bh * kCuts + threadIdx.x];
+  }
+  __syncthreads();
   // the histogram slots of this pass, fixed before any cut's prefix changes
   int slot[kCuts];
   uint64_t pre[kCuts];
-  hist_slots(args, bh, s + kWidth[pass], slot, pre);
+  slots_of(s_prefix, s_kleft, s + kWidth[pass], slot, pre);
   uint32_t ncand[kCuts];
   for (int t = 0; t < kCuts; ++t)
     ncand[t] = pass == kCollectPass && slot[t] >= 0 ? args.ccount[bh * kCuts + slot[t]] : (uint32_t)kRankCand + 1u;
-  __syncthreads();  // every thread has read the counts and prefixes before any changes
+  __syncthreads();  // every thread has read the prefixes and ranks before any changes
   for (int t = 0; t < kCuts; ++t) {
-    const int64_t k = args.kleft[bh * kCuts + t];
+    const int64_t k = s_kleft[t];
     if (k <= 0) continue;  // uniform across the block
     if (ncand[t] >= 1u && ncand[t] <= (uint32_t)kRankCand && k <= (int64_t)ncand[t]) {
       // the collected keys are exactly those with this cut's prefix, and the
@@ -206,38 +265,53 @@ __global__ __launch_bounds__(256) void rank_scan_kernel(RankArgs args, int pass)
       __syncthreads();
       block_sort_desc(sk, np);
       if (threadIdx.x == 0) {
-        args.prefix[bh * kCuts + t] = sk[k - 1];
-        args.kleft[bh * kCuts + t] = 0;
+        s_prefix[t] = sk[k - 1];
+        s_kleft[t] = 0;
       }
       __syncthreads();
       continue;
     }
-    // thread i owns bins [2047-8i-7, 2047-8i], visited from the top
-    uint32_t c[8], local = 0;
-    for (int q = 0; q < 8; ++q) {
-      c[q] = gh[slot[t] * kBins + (kBins - 1 - 8 * threadIdx.x - q)];
-      local += c[q];
-    }
-    uint32_t total;
-    uint32_t before = block_exscan_256(local, sh, &total);
-    if ((int64_t)before < k && k <= (int64_t)before + local) {
-      uint32_t run = before;
-      for (int q = 0; q < 8; ++q) {
-        if (k <= (int64_t)run + c[q]) {
-          const uint64_t dig = kBins - 1 - 8 * threadIdx.x - q;
-          args.prefix[bh * kCuts + t] |= dig << s;
-          args.kleft[bh * kCuts + t] = k - run;
-          break;
-        }
-        run += c[q];
-      }
-    }
-    __syncthreads();
+    scan_digit(gh + slot[t] * kBins, s, k, s_prefix[t], s_kleft[t], sh);
   }
   for (int i = threadIdx.x; i < kCuts * kBins; i += 256) gh[i] = 0u;
-  if (pass == kPasses - 1 && threadIdx.x < kCuts) {
+  if (pass == kCollectPass) {
+    // remaining passes for the cuts still open, in this workgroup (the
+    // candidate sorts are done with sk, whose LDS now holds the histograms)
+    uint32_t* lh = reinterpret_cast<uint32_t*>(sk);
+    static_assert(kCuts * kBins * sizeof(uint32_t) <= sizeof(sk), "histograms fit");
+    const int64_t M = (int64_t)args.R * args.R;
+    const float* A = args.A + (int64_t)bh * M;
+    for (int q = kCollectPass + 1; q < kPasses; ++q) {
+      bool open = false;
+      for (int t = 0; t < kCuts; ++t) open = open || s_kleft[t] > 0;
+      if (!open) break;  // uniform: every thread reads the same LDS values
+      const int sq = kShift[q], hi = sq + kWidth[q];
+      const uint64_t mask = (1ull << kWidth[q]) - 1ull;
+      slots_of(s_prefix, s_kleft, hi, slot, pre);
+      bool own[kCuts];
+      for (int t = 0; t < kCuts; ++t) own[t] = slot[t] == t;
+      for (int i = threadIdx.x; i < kCuts * kBins; i += 256) lh[i] = 0u;
+      __syncthreads();
+      for (int64_t e = threadIdx.x; e < M; e += 256) {
+        const uint64_t key = rank_key(A[e], static_cast<uint32_t>(e));
+        const uint32_t dig = static_cast<uint32_t>((key >> sq) & mask);
+        for (int t = 0; t < kCuts; ++t)
+          if (own[t] && (key >> hi) == pre[t]) atomicAdd(&lh[t * kBins + dig], 1u);
+      }
+      __syncthreads();
+      for (int t = 0; t < kCuts; ++t) {
+        const int64_t k = s_kleft[t];
+        if (k <= 0) continue;  // uniform
+        scan_digit(lh + slot[t] * kBins, sq, k, s_prefix[t], s_kleft[t], sh);
+      }
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < kCuts) {
     const int t = threadIdx.x;
-    args.thr[bh * kCuts + t] = args.cut[t] > 0 ? args.prefix[bh * kCuts + t] : kNone;
+    args.prefix[bh * kCuts + t] = s_prefix[t];
+    args.kleft[bh * kCuts + t] = s_kleft[t];
+    if (pass == kCollectPass) args.thr[bh * kCuts + t] = args.cut[t] > 0 ? s_prefix[t] : kNone;
   }
 }
 
@@ -466,7 +540,8 @@ hipError_t launch_rank(const RankArgs& args, hipStream_t stream) {
     const int64_t M = (int64_t)args.R * args.R;
     const int chunks = (int)((M + kHistChunk - 1) / kHistChunk);
     hipLaunchKernelGGL(rank_init_kernel, dim3(BH), dim3(256), 0, stream, args);
-    for (int p = 0; p < kPasses; ++p) {
+    // passes after the collecting one run inside its scan (see rank_scan_kernel)
+    for (int p = 0; p <= kCollectPass; ++p) {
       hipLaunchKernelGGL(rank_hist_kernel, dim3(chunks, BH), dim3(256), 0, stream, args, p);
       hipLaunchKernelGGL(rank_scan_kernel, dim3(BH), dim3(256), 0, stream, args, p);
     }
