@@ -118,7 +118,7 @@ constexpr float kLog2_2688 = 11.392317422778760f;  // log2(6 * 448)
 struct Fp4Group {
   float off, scale, sum;
   f16x2 s2;
-  uint32_t code[2];  // E2M1 codes of slots [0,8) and [8,16), two per byte
+  uint32_t code[2];  // E2M1 codes of slots [0,8) and [8,16), two per byte (written by fp4_exp_pair)
 };
 // E4M3 value of a in [0, 448]: v_cvt_pk_fp8_f32 rounds to nearest even (the
 // device format tests check it against the format definition on that range)
@@ -135,7 +135,6 @@ __device__ inline void fp4_setup(Fp4Group& G, float gmax, float c, float mn) {
   const _Float16 sh = (_Float16)sigma;
   G.s2 = f16x2{sh, sh};
   G.sum = 0.0f;
-  G.code[0] = G.code[1] = 0u;
 }
 // Weights of slots [I0, I1) (I0, I1 even): y = 2^(S c + off) from one exp2
 // each, added to the fp32 sum and converted to E2M1 in pairs right away.
@@ -145,7 +144,11 @@ __device__ inline void fp4_exp_pair(Fp4Group& G, const f32x16& S, float c) {
   const float y1 = exp2_fast(__builtin_fmaf(S[I + 1], c, G.off));
   G.sum += y0;
   G.sum += y1;
-  G.code[I >> 3] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(G.code[I >> 3], y0, y1, 1.0f, (I >> 1) & 3);
+  // pairs are converted in ascending order, so byte 0 is the first byte
+  // written in each code word: its conversion may keep anything in the other
+  // bytes (the bits of an input that dies here; no register is cleared)
+  const uint32_t kept = ((I >> 1) & 3) == 0 ? __float_as_uint(y1) : G.code[I >> 3];
+  G.code[I >> 3] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(kept, y0, y1, 1.0f, (I >> 1) & 3);
 }
 template <int I0, int I1>
 __device__ inline void fp4_exps(Fp4Group& G, const f32x16& S, float c) {
@@ -184,8 +187,11 @@ __device__ inline float fp8_weights8(const f32x16& S, float cb, float off, int& 
     p[e] = exp2_fast(__builtin_fmaf(S[I0 + e], cb, off));
     sum += p[e];
   }
-  w0 = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], 0, false), true);
-  w1 = __builtin_amdgcn_cvt_pk_fp8_f32(p[6], p[7], __builtin_amdgcn_cvt_pk_fp8_f32(p[4], p[5], 0, false), true);
+  // the high half of each word's first conversion is overwritten by the
+  // second, so its kept half may be anything: the bits of an input that dies
+  // here, which needs no register cleared for it
+  w0 = __builtin_amdgcn_cvt_pk_fp8_f32(p[2], p[3], __builtin_amdgcn_cvt_pk_fp8_f32(p[0], p[1], __float_as_int(p[1]), false), true);
+  w1 = __builtin_amdgcn_cvt_pk_fp8_f32(p[6], p[7], __builtin_amdgcn_cvt_pk_fp8_f32(p[4], p[5], __float_as_int(p[5]), false), true);
   return sum;
 }
 
@@ -231,7 +237,9 @@ __device__ inline int mx_codes8(const f32x16& S, float c, float off, float& sum)
     y[e] = exp2_fast(__builtin_fmaf(S[I0 + e], c, off));
     sum += y[e];
   }
-  uint32_t w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, y[0], y[1], 1.0f, 0);
+  // bytes 1-3 are written below, so byte 0's conversion may keep anything
+  // there: the bits of an input that dies here
+  uint32_t w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(__float_as_uint(y[1]), y[0], y[1], 1.0f, 0);
   w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[2], y[3], 1.0f, 1);
   w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[4], y[5], 1.0f, 2);
   w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, y[6], y[7], 1.0f, 3);
