@@ -124,7 +124,8 @@ struct Fp4Group {
 // device format tests check it against the format definition on that range)
 // and v_cvt_f32_fp8 returns the exact value.
 __device__ inline float e4m3_round_hw(float a) {
-  return __builtin_amdgcn_cvt_f32_fp8(__builtin_amdgcn_cvt_pk_fp8_f32(a, 0.0f, 0, false), 0);
+  // only byte 0 is read back, so the kept bytes may be anything: a's bits
+  return __builtin_amdgcn_cvt_f32_fp8(__builtin_amdgcn_cvt_pk_fp8_f32(a, 0.0f, __float_as_int(a), false), 0);
 }
 __device__ inline void fp4_setup(Fp4Group& G, float gmax, float c, float mn) {
   const float pmax = exp2_fast(__builtin_fmaf(gmax, c, -mn));
