@@ -452,25 +452,37 @@ __global__ __launch_bounds__(NT) void rank_classify_kernel(RankArgs args) {
 // one contiguous segment (about n/8 rows of one or two heads, whose K/V then
 // share that XCD's L2) longest-first.
 constexpr int kOrderBins = 8192;
-__device__ inline int order_key(const RankArgs& args, int64_t i) {
-  const int BH = args.B * args.H;
-  const int64_t cmax = 3ll * args.R;  // cost of a row with R 4-bit or 16-bit blocks
-  const int groups = 2 * BH;
-  const int nbh = groups < kOrderBins ? kOrderBins / groups : 1;  // cost bins per group
-  const int bh = (int)(i / args.R), half = (int)(i % args.R) & 1;
-  const int bin = (int)((int64_t)args.cost[i] * (nbh - 1) / (cmax > 0 ? cmax : 1));
-  int64_t key = (int64_t)(2 * bh + half) * nbh + (nbh - 1 - bin);
-  if ((int64_t)groups * nbh > kOrderBins) key = key * kOrderBins / ((int64_t)groups * nbh);
-  return (int)key;
+// Bin of row i (cost c) in the work order. 32-bit arithmetic: rows number
+// fewer than 2^31 and R <= 65535 (both checked on the host), so c (n4 + n8 +
+// n16 <= R blocks at most 3 each) times the bins per group (<= 4096) and the
+// rescaled key (< 2^16 x 8192) stay below 2^32.
+__device__ inline uint32_t order_key(const RankArgs& args, uint32_t i, int32_t c) {
+  const uint32_t R = static_cast<uint32_t>(args.R), BH = static_cast<uint32_t>(args.B * args.H);
+  const uint32_t cmax = 3u * R;  // cost of a row with R 4-bit or 16-bit blocks
+  const uint32_t groups = 2u * BH;
+  const uint32_t nbh = groups < kOrderBins ? kOrderBins / groups : 1u;  // cost bins per group
+  const uint32_t bh = i / R, half = (i - bh * R) & 1u;
+  const uint32_t bin = static_cast<uint32_t>(c) * (nbh - 1u) / cmax;
+  uint32_t key = (2u * bh + half) * nbh + (nbh - 1u - bin);
+  if (groups * nbh > kOrderBins) key = key * kOrderBins / (groups * nbh);
+  return key;
 }
 
 __global__ __launch_bounds__(1024) void rank_order_kernel(RankArgs args) {
   __shared__ uint32_t hist[kOrderBins];
   __shared__ uint32_t part[1024];
-  const int64_t n = (int64_t)args.B * args.H * args.R;
+  constexpr int U = 8;  // row costs in flight per thread
+  const uint32_t n = static_cast<uint32_t>(args.B * args.H) * static_cast<uint32_t>(args.R);
   for (int i = threadIdx.x; i < kOrderBins; i += 1024) hist[i] = 0u;
   __syncthreads();
-  for (int64_t i = threadIdx.x; i < n; i += 1024) atomicAdd(&hist[order_key(args, i)], 1u);
+  for (uint32_t i0 = threadIdx.x; i0 < n; i0 += 1024u * U) {
+    int32_t c[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) c[u] = args.cost[min(i0 + 1024u * u, n - 1u)];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (i0 + 1024u * u < n) atomicAdd(&hist[order_key(args, i0 + 1024u * u, c[u])], 1u);
+  }
   __syncthreads();
   constexpr int per = kOrderBins / 1024;
   uint32_t s = 0;
@@ -493,12 +505,21 @@ __global__ __launch_bounds__(1024) void rank_order_kernel(RankArgs args) {
     run += v;
   }
   __syncthreads();
-  for (int64_t i = threadIdx.x; i < n; i += 1024) {
-    const uint32_t pos = atomicAdd(&hist[order_key(args, i)], 1u);
-    args.order[pos] = (int32_t)i;
+  for (uint32_t i0 = threadIdx.x; i0 < n; i0 += 1024u * U) {
+    int32_t c[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) c[u] = args.cost[min(i0 + 1024u * u, n - 1u)];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = i0 + 1024u * u;
+      if (i < n) {
+        const uint32_t pos = atomicAdd(&hist[order_key(args, i, c[u])], 1u);
+        args.order[pos] = static_cast<int32_t>(i);
+      }
+    }
   }
   if (threadIdx.x == 0) {
-    args.meta[0] = (int32_t)n;
+    args.meta[0] = static_cast<int32_t>(n);
     args.meta[1] = 0;  // error flags of da2_mixed_attn calls on these lists
   }
 }
