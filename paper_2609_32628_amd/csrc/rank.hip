@@ -52,13 +52,16 @@ __global__ void rank_init_kernel(RankArgs args) {
   }
 }
 
-// Histogram slot of each cut in this pass: -1 for a finished cut, else the
-// first active cut with the same prefix (cuts with equal prefixes, such as all
-// of them in the first pass, count the same elements into one histogram).
-__device__ inline void hist_slots(const RankArgs& args, int bh, int hi, int (&slot)[kCuts], uint64_t (&pre)[kCuts]) {
+// Histogram slot of each cut in the pass whose digit ends at bit hi: -1 for a
+// finished cut, else the first active cut with the same prefix (cuts with
+// equal prefixes, such as all of them in the first pass, count the same
+// elements into one histogram). prefix and kleft: the head's cuts, in global
+// memory or LDS.
+__device__ inline void slots_of(const uint64_t* prefix, const int64_t* kleft, int hi, int (&slot)[kCuts],
+                                uint64_t (&pre)[kCuts]) {
   for (int t = 0; t < kCuts; ++t) {
-    pre[t] = args.prefix[bh * kCuts + t] >> hi;
-    slot[t] = args.kleft[bh * kCuts + t] > 0 ? t : -1;
+    pre[t] = prefix[t] >> hi;
+    slot[t] = kleft[t] > 0 ? t : -1;
     for (int u = 0; u < t && slot[t] == t; ++u)
       if (slot[u] == u && pre[u] == pre[t]) slot[t] = u;
   }
@@ -76,7 +79,7 @@ __global__ __launch_bounds__(256) void rank_hist_kernel(RankArgs args, int pass)
   for (int i = threadIdx.x; i < kCuts * kBins; i += 256) (&lh[0][0])[i] = 0u;
   int slot[kCuts];
   uint64_t pre[kCuts];
-  hist_slots(args, bh, hi, slot, pre);
+  slots_of(args.prefix + bh * kCuts, args.kleft + bh * kCuts, hi, slot, pre);
   bool own[kCuts], any = false;
   for (int t = 0; t < kCuts; ++t) {
     own[t] = slot[t] == t;
@@ -206,18 +209,6 @@ __device__ inline void scan_digit(const uint32_t* h, int s, int64_t k, uint64_t&
     }
   }
   __syncthreads();
-}
-
-// Histogram slots of the pass whose digit ends at bit hi, from the cuts'
-// prefixes and ranks left (the same rule as hist_slots).
-__device__ inline void slots_of(const uint64_t* prefix, const int64_t* kleft, int hi, int (&slot)[kCuts],
-                                uint64_t (&pre)[kCuts]) {
-  for (int t = 0; t < kCuts; ++t) {
-    pre[t] = prefix[t] >> hi;
-    slot[t] = kleft[t] > 0 ? t : -1;
-    for (int u = 0; u < t && slot[t] == t; ++u)
-      if (slot[u] == u && pre[u] == pre[t]) slot[t] = u;
-  }
 }
 
 // One workgroup per head: fixes this pass's digit of every cut from the
