@@ -201,6 +201,40 @@ __device__ inline double wave_max_f64(double v) {
   return v;
 }
 
+// e^x for x <= 0 in float64: Cody-Waite range reduction x = k ln2 + r with
+// |r| <= ln2/2 (two multiply-adds, ln2 split into its nearest double and the
+// remainder), then the Taylor series of e^r to degree 13 in Horner form (the
+// truncation error is below 5e-18 relative on that interval) and ldexp(., k).
+// The coefficients are 1/n! rounded to the nearest double; they live in
+// constant memory, so the multiply-adds read them from scalar registers
+// instead of copying each into a vector register first. Inputs below -746
+// give 0, like e^x itself in float64.
+__constant__ double kExpTaylor[14] = {1.0,
+                                      1.0,
+                                      0.5,
+                                      0.16666666666666666,
+                                      0.041666666666666664,
+                                      0.008333333333333333,
+                                      0.001388888888888889,
+                                      0.0001984126984126984,
+                                      2.48015873015873e-05,
+                                      2.7557319223985893e-06,
+                                      2.755731922398589e-07,
+                                      2.505210838544172e-08,
+                                      2.08767569878681e-09,
+                                      1.6059043836821613e-10};
+__device__ inline double exp_neg(double x) {
+  constexpr double kLog2e = 1.4426950408889634, kLn2Hi = 0.6931471805599453, kLn2Lo = 2.3190468138462996e-17;
+  x = fmax(x, -746.0);
+  const double k = rint(x * kLog2e);
+  double r = fma(-k, kLn2Hi, x);
+  r = fma(-k, kLn2Lo, r);
+  double p = kExpTaylor[13];
+#pragma unroll
+  for (int n = 12; n >= 0; --n) p = fma(p, r, kExpTaylor[n]);
+  return ldexp(p, static_cast<int>(k));
+}
+
 // One wave per row of A (four rows per workgroup): the two row softmaxes (max
 // subtracted) mixed with weight lambda, rounded once to float32. Rows of up to
 // 64 KMAX entries keep their logits and exponentials in registers (one exp per
@@ -228,8 +262,8 @@ __global__ __launch_bounds__(256) void draft_softmax_reg_kernel(DraftArgs args) 
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) {
     const bool in = lane + 64 * k < R;
-    e1[k] = in ? exp(e1[k] - m1) : 0.0;
-    e2[k] = in ? exp(e2[k] - m2) : 0.0;
+    e1[k] = in ? exp_neg(e1[k] - m1) : 0.0;
+    e2[k] = in ? exp_neg(e2[k] - m2) : 0.0;
     z1 += e1[k];
     z2 += e2[k];
   }
@@ -262,15 +296,15 @@ __global__ __launch_bounds__(256) void draft_softmax_kernel(DraftArgs args) {
   m2 = wave_max_f64(m2);
   double z1 = 0.0, z2 = 0.0;
   for (int i = lane; i < R; i += 64) {
-    z1 += exp(s1[i] - m1);
-    z2 += exp(s2[i] - m2);
+    z1 += exp_neg(s1[i] - m1);
+    z2 += exp_neg(s2[i] - m2);
   }
   z1 = wave_sum_f64(z1);
   z2 = wave_sum_f64(z2);
   const double lam = args.lambda;
   const double r1 = (1.0 - lam) / z1, r2 = lam / z2;
   float* out = args.A + row * R;
-  for (int i = lane; i < R; i += 64) out[i] = (float)(exp(s1[i] - m1) * r1 + exp(s2[i] - m2) * r2);
+  for (int i = lane; i < R; i += 64) out[i] = (float)(exp_neg(s1[i] - m1) * r1 + exp_neg(s2[i] - m2) * r2);
 }
 
 hipError_t launch_draft(const DraftArgs& args, hipStream_t stream) {
