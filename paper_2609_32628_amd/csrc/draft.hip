@@ -208,7 +208,7 @@ __device__ inline double wave_max_f64(double v) {
 // The coefficients are 1/n! rounded to the nearest double; they live in
 // constant memory, so the multiply-adds read them from scalar registers
 // instead of copying each into a vector register first. Inputs below -746
-// give 0, like e^x itself in float64.
+// give 0, like e^x itself in float64; a NaN gives NaN.
 __constant__ double kExpTaylor[14] = {1.0,
                                       1.0,
                                       0.5,
@@ -225,7 +225,7 @@ __constant__ double kExpTaylor[14] = {1.0,
                                       1.6059043836821613e-10};
 __device__ inline double exp_neg(double x) {
   constexpr double kLog2e = 1.4426950408889634, kLn2Hi = 0.6931471805599453, kLn2Lo = 2.3190468138462996e-17;
-  x = fmax(x, -746.0);
+  x = x < -746.0 ? -746.0 : x;  // (a NaN stays NaN)
   const double k = rint(x * kLog2e);
   double r = fma(-k, kLn2Hi, x);
   r = fma(-k, kLn2Lo, r);
