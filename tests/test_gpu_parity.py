@@ -114,6 +114,33 @@ def test_draft_map_row_lengths(w):
         assert stats[bh, 1] == np.float32(np.abs(K[0, bh]).max()).view(np.uint32)
 
 
+# Wide logit range: Q and K scaled by 8 (exact in bf16) make the max-pooled
+# logits of a row span thousands of units, so many e^(s - m) underflow in
+# float64 (below e^-745) and many more round to zero in the float32 A; the
+# GPU's exponential must agree with the oracle's there as well.
+def test_draft_map_wide_logit_range():
+    w = replace(configs.MID, name="draft-21x30x52-h2-x8", H=2)
+    log(f"draft_map parity {w.name}")
+    Q, K, V = inputs(w)
+    Q, K = Q * 8.0, K * 8.0
+    p = problem_of(w)
+    buf = api.alloc(p, w.scope)
+    api.da2_draft_map(to_device(Q, w), to_device(K, w), buf.layout, p, w.lam, buf.A, buf.stats, buf.ws_draft)
+    torch.cuda.synchronize()
+    slot2tok, n_a, _ = partition.make_partition(w.partition, w.T, w.Hg, w.Wg)
+    R = n_a.size
+    A = buf.A.cpu().numpy().reshape(-1, R, R)
+    for bh in range(A.shape[0]):
+        A32, pl = odraft.draft_head(Q[0, bh], K[0, bh], slot2tok, n_a, w.lam)
+        span = np.ptp(pl["Qmax"] @ pl["Kmax"].T / np.sqrt(w.d), axis=1).max()
+        zeros = (A32 == 0).sum()
+        rel = np.abs(A[bh].astype(np.float64) - A32) / np.maximum(A32, 1e-30)
+        log(f"  head {bh}: logit span {span:.0f}, oracle zeros {zeros}, A max rel diff {rel.max():.2e}")
+        assert span > 745 and zeros > 0  # the case this test is for
+        assert np.array_equal(A[bh] == 0, A32 == 0)
+        assert rel.max() <= 1e-6
+
+
 def _tie_heavy(R, seed):
     rng = np.random.default_rng(seed)
     A = rng.random((R, R)).astype(np.float32)
